@@ -1,0 +1,199 @@
+/*
+ * libsplash_attn -- owner-local paged MLA decode attention for MI355X (gfx950).
+ *
+ * The operation (Sec. 3 "DOP: Computation"; Sec. 3 "Cost"; App. B "Per-Step
+ * Cost Model"): an owner GPU holds its N_r = B*q current query rows for all H
+ * heads, [N_r, H, d_q] with d_q = d_c + d_r = 576, and the whole latent history
+ * of each request it owns, kept in pages.  For every row and every head it
+ * attends over the complete causal prefix of that request's history (Sec. 4.1
+ * "Handoff") and returns a d_z = d_c = 512 wide output per head.  MLA keeps one
+ * head-shared latent row per token (Sec. 1), so one cache row [latent 512 |
+ * rope 64] serves as the key of every head, and its first 512 entries serve as
+ * the value.  DP-attention and DOP run this same owner-local core (App. B).
+ *
+ * For request b with history length s_b (s_b counts the current chunk,
+ * 1 <= q_chunk <= s_b), chunk row i and head h, output row n = b*q_chunk + i:
+ *   visible keys j = 0 .. s_b - q_chunk + i
+ *   K_j  = pool row  block_table[b*max_pages_per_seq + j/64]*64 + j%64
+ *          (fp8 cache: K_j = e4m3(code) * kv_scales[that row])
+ *   z_j  = softmax_scale * <q[n,h,:], K_j>
+ *   lse[n,h]   = ln sum_j exp(z_j)                (natural log, scaled logits)
+ *   out[n,h,:] = sum_j exp(z_j - lse[n,h]) * K_j[0:512]
+ *
+ * Conventions for every entry point:
+ *  - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates or frees device memory in these calls and keeps no
+ *    pointer after it returns.  `stream` is a hipStream_t (NULL: the null
+ *    stream); all work is enqueued on it with no host synchronisation (except
+ *    under SPLASH_FLAG_DEBUG_CHECK), so the calls can be captured in a graph.
+ *  - Return value: SPLASH_OK or a negative status; no C++ exception crosses
+ *    the boundary.  splash_status_string() names a status and
+ *    splash_last_error() holds the last detailed message of the calling
+ *    thread.
+ *  - Device data is trusted on the fast path: seq_lens[b] < q_chunk or a
+ *    block-table entry outside [0, num_pages) is undefined behaviour unless
+ *    SPLASH_FLAG_DEBUG_CHECK is set, which validates them first.
+ *  - Unused block-table slots (past ceil(s_b/64)) and pool rows past a
+ *    history's end are never used in the result.
+ */
+#ifndef SPLASH_ATTN_H
+#define SPLASH_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes -------------------------------------------------------- */
+#define SPLASH_OK                        0
+#define SPLASH_ERR_INVALID_ARGUMENT     (-1) /* null pointer, q_chunk<1, dims != 576/512, bad scale, bad device data */
+#define SPLASH_ERR_UNSUPPORTED          (-2) /* H not in {16,32,...,128}, page size != 64, unknown kv dtype */
+#define SPLASH_ERR_MISALIGNED           (-3) /* a tensor base pointer not 16-byte aligned */
+#define SPLASH_ERR_WORKSPACE_TOO_SMALL  (-4)
+#define SPLASH_ERR_HIP                  (-5) /* a HIP call or launch failed; see splash_last_error() */
+
+/* ---- cache formats --------------------------------------------------------- */
+#define SPLASH_KV_BF16      0  /* pool: [num_pages, 64, 576] bf16 */
+#define SPLASH_KV_FP8_E4M3  1  /* pool: [num_pages, 64, 576] OCP E4M3 ("fn") bytes + kv_scales [num_pages, 64] fp32 */
+
+/* ---- flags ------------------------------------------------------------------ */
+#define SPLASH_FLAG_DEBUG_CHECK  1u  /* validate seq_lens / block table on the device first; synchronises `stream` */
+#define SPLASH_FLAG_FORCE_SPLIT  2u  /* split every history into work units of `split_pages` pages */
+
+#define SPLASH_DIM_QK     576
+#define SPLASH_DIM_V      512
+#define SPLASH_PAGE_SIZE  64
+#define SPLASH_MAX_HEADS  128
+
+/* Description of one call.  Sizes are element counts. */
+typedef struct splash_mla_desc {
+    int32_t batch;              /* B: requests owned by this GPU (0: idle owner, every call is a no-op) */
+    int32_t num_heads;          /* H: query heads, a multiple of 16 in [16, 128] */
+    int32_t dim_qk;             /* must be 576 = 512 latent + 64 rope */
+    int32_t dim_v;              /* must be 512 */
+    int32_t page_size;          /* must be 64 */
+    int32_t max_pages_per_seq;  /* row stride of block_table (>= ceil(max s_b / 64)) */
+    int32_t num_pages;          /* pages in the pool */
+    int32_t kv_dtype;           /* SPLASH_KV_* */
+    const float* kv_scales;     /* device [num_pages, 64] fp32 per-token scales; FP8 only, else ignored */
+    float softmax_scale;        /* multiplies <q, k>; finite and > 0 (1/sqrt(192) for DeepSeek-V3 dims) */
+    uint32_t flags;             /* SPLASH_FLAG_* */
+    int32_t split_pages;        /* with SPLASH_FLAG_FORCE_SPLIT: pages per work unit, >= 1 */
+} splash_mla_desc;
+
+/*
+ * Workspace.  One caller-allocated device buffer carries the plan (work list,
+ * split offsets) and the fp32 partial results of split histories.
+ * `max_partials` bounds how many partial results (one per work unit of a
+ * split history, H x 512 fp32 each) the planner may use; <= 0 selects
+ * SPLASH_DEFAULT_MAX_PARTIALS.  The planner never exceeds the capacity that
+ * the passed ws_bytes provides: with too little room it splits less.
+ * Layout (byte offsets from splash_mla_workspace_offsets, 256-byte aligned):
+ *   [0] header int32[64]: [0] unit counter, [1] number of work units,
+ *       [2] partial slots used, [3] pages per unit chosen, [4] debug status
+ *   [1] work units int32[max_units][4] = {tile, first page, end page, slot},
+ *       tile = b*q_chunk + i, slot = partial index or -1 (unit writes out/lse)
+ *   [2] split offsets int32[B*q_chunk + 1] (partial slots of tile t are
+ *       [off[t], off[t+1]); empty when the tile is a single unit)
+ *   [3] partial lse fp32 [max_partials, H]
+ *   [4] partial out fp32 [max_partials, H, 512]
+ */
+#define SPLASH_DEFAULT_MAX_PARTIALS 1024
+size_t splash_mla_workspace_size(int32_t batch, int32_t q_chunk, int32_t num_heads,
+                                 int32_t max_partials);
+/* Writes the five byte offsets above into offsets[5]; returns the total size. */
+size_t splash_mla_workspace_offsets(int32_t batch, int32_t q_chunk, int32_t num_heads,
+                                    int32_t max_partials, size_t* offsets);
+
+/*
+ * splash_mla_attend: the whole step -- plan, attend, combine -- on `stream`.
+ *   q            bf16 [B*q_chunk, H, 576], row n = b*q_chunk + i, each head's 576
+ *                entries packed [no-position 512 | rotary 64] (App. D)
+ *   kv_pages     pool, see SPLASH_KV_*
+ *   block_table  int32 [B, max_pages_per_seq]; logical page k of request b is
+ *                physical page block_table[b*max_pages_per_seq + k]
+ *   seq_lens     int32 [B], history length including the current chunk
+ *   q_chunk      query rows per request (1: decode), 1 <= q_chunk <= seq_lens[b]
+ *   out          bf16 [B*q_chunk, H, 512] (round to nearest even)
+ *   lse          fp32 [B*q_chunk, H] natural-log LSE of the scaled logits; may be NULL
+ * Results are deterministic: the same inputs give the same bits, independent
+ * of page placement in the pool and of how units land on compute units.
+ */
+int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_table,
+                      const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
+                      const splash_mla_desc* desc, void* workspace, size_t ws_bytes,
+                      void* stream);
+
+/*
+ * splash_mla_plan + splash_mla_run: the same step in two halves, so that a
+ * plan made once per step (it depends only on seq_lens, q_chunk and desc) can
+ * serve every layer.  splash_mla_run must see the workspace of a plan made
+ * with the same seq_lens, q_chunk and desc, earlier in stream order.
+ * The split heuristic (a cost-model argmin over candidate unit sizes, in the
+ * spirit of Sec. 4.2's calibrated argmin) balances pages over the compute
+ * units and splits a history only where that shortens the step.
+ */
+int splash_mla_plan(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* desc,
+                    void* workspace, size_t ws_bytes, void* stream);
+int splash_mla_run(const void* q, const void* kv_pages, const int32_t* block_table,
+                   const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
+                   const splash_mla_desc* desc, void* workspace, size_t ws_bytes,
+                   void* stream);
+
+/*
+ * splash_mla_combine: merge partial attention results over disjoint key sets
+ * into the result over their union (the merge a position-sharded history
+ * needs, App. D).  For request b, partial slots s in
+ * [split_indptr[b], split_indptr[b+1]) each hold rows i < q_chunk:
+ *   partials     fp32 [S_tot, q_chunk, H, 512], normalised outputs
+ *   partial_lse  fp32 [S_tot, q_chunk, H]; -inf marks a part with no key
+ *   L = ln sum_s exp(lse_s);  out = sum_s exp(lse_s - L) * partial_s
+ *   out          bf16 [B*q_chunk, H, 512]; out_lse fp32 [B*q_chunk, H] or NULL
+ * A request with no partial, or whose parts are all -inf, gets out = 0 and
+ * lse = -inf.  split_indptr is a device int32 [B+1] array.
+ */
+int splash_mla_combine(const float* partials, const float* partial_lse,
+                       const int32_t* split_indptr, int32_t batch, int32_t q_chunk,
+                       int32_t num_heads, void* out, float* out_lse, void* stream);
+
+/*
+ * splash_mla_debug_gather (tests): copy every history, token by token, into
+ * a dense buffer through the same page-address code the attention kernel
+ * uses.  dense_out holds sum_b seq_lens[b] rows of the pool's row bytes
+ * (1152 for bf16, 576 for fp8), request after request.
+ */
+int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table,
+                            const int32_t* seq_lens, const splash_mla_desc* desc,
+                            void* dense_out, void* stream);
+
+/*
+ * splash_mla_plan_host: the planner run on the CPU over HOST seq_lens, for
+ * tests and for callers that want to inspect a plan.  It computes exactly
+ * what splash_mla_plan computes on the device for `num_workers` compute units
+ * and `max_partials` partial slots.  units_out: int32 [max_units][4];
+ * indptr_out: int32 [B*q_chunk + 1]; stats_out: int32[4] = {units, partial
+ * slots used, pages per unit, total pages}.  Returns SPLASH_OK, or
+ * SPLASH_ERR_WORKSPACE_TOO_SMALL when max_units is too small.
+ */
+int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk,
+                         const splash_mla_desc* desc, int32_t num_workers,
+                         int32_t max_partials, int32_t* units_out, int32_t max_units,
+                         int32_t* indptr_out, int32_t* stats_out);
+
+/* Number of work units the workspace reserves: B*q_chunk + max_partials. */
+int32_t splash_mla_max_units(int32_t batch, int32_t q_chunk, int32_t max_partials);
+
+/* Compute units of the current device as the planner sees them (>= 1). */
+int32_t splash_device_workers(void);
+
+const char* splash_status_string(int status);
+const char* splash_last_error(void);
+const char* splash_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPLASH_ATTN_H */

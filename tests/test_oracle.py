@@ -1,0 +1,274 @@
+"""The fp64 oracle against its pins (CPU only).
+
+Pins come from outside the oracle: format definitions cross-checked with
+numpy/torch dtypes and the OCP table, brute force over dense un-paged inputs,
+torch's float64 scaled-dot-product attention, closed forms, invariants and a
+hand-worked example.  The mutation tests plant plausible mistakes in the
+oracle (on the CPU) and require that some pin catches each one.
+"""
+import contextlib
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.formats
+import oracle.mla
+from tests import oracle_pins as pins
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TOL = 1e-12
+
+
+# ---------------------------------------------------------------- formats ---
+
+def test_bf16_decode_all_patterns_match_binary32_upper_half():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    mine = oracle.bf16_bits_to_f64(bits)
+    ref = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+
+
+def test_e4m3_decode_all_patterns_match_torch_float8_e4m3fn():
+    bits = np.arange(256, dtype=np.uint8)
+    mine = oracle.e4m3_bits_to_f64(bits)
+    ref = torch.from_numpy(bits.copy()).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(mine[~nan]), np.signbit(ref[~nan]))
+
+
+def test_e4m3_decode_ocp_anchor_values():
+    for line in open(os.path.join(GOLDEN, "e4m3_anchor_values.txt")):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        code, val = line.split()
+        got = oracle.e4m3_bits_to_f64(np.array([int(code, 16)], dtype=np.uint8))[0]
+        if val == "nan":
+            assert math.isnan(got)
+        else:
+            assert got == float(val) and math.copysign(1, got) == math.copysign(1, float(val))
+
+
+# -------------------------------------------------------------- attention ---
+
+def test_matches_brute_force_dense_unpaged():
+    assert pins.pin_brute_force() <= TOL
+
+
+def test_matches_brute_force_decode_rows():
+    assert pins.pin_brute_force(seed=9, B=2, H=3, q_chunk=1, s_max=129) <= TOL
+
+
+def test_matches_torch_sdpa_float64_with_causal_chunk_mask():
+    assert pins.pin_sdpa() <= 1e-12
+
+
+def test_fp8_cache_matches_sdpa_on_dequantised_rows():
+    assert pins.pin_fp8_dequant() <= 1e-12
+
+
+def test_single_key_returns_its_latent():
+    assert pins.pin_single_key() == 0.0
+
+
+def test_zero_query_gives_mean_of_visible_values():
+    assert pins.pin_zero_query() <= TOL
+
+
+def test_equal_logits_over_distinct_latents():
+    assert pins.pin_shared_rope_distinct_latents() <= TOL
+
+
+@pytest.mark.parametrize("target", [0, 63, 64, 70, 129])
+def test_dominant_logit_selects_one_token(target):
+    assert pins.pin_one_hot(target) <= TOL
+
+
+def test_softmax_rows_sum_to_one():
+    assert pins.pin_probs_sum_to_one() <= TOL
+
+
+def test_physical_page_permutation_is_bit_identical():
+    assert pins.pin_page_permutation() == 0.0
+
+
+def test_chunk_rows_equal_single_token_decodes():
+    assert pins.pin_chunk_rows_are_decodes() <= TOL
+
+
+def test_head_and_request_subsets_are_independent():
+    assert pins.pin_head_and_request_partition() <= 1e-13
+
+
+def test_merge_of_key_partition_equals_whole():
+    assert pins.pin_merge_identity() <= TOL
+
+
+def test_merge_of_only_empty_parts_is_empty():
+    out, lse = oracle.merge_partials(np.zeros((3, 2, 512)), np.full((3, 2), -np.inf))
+    assert np.all(np.isneginf(lse)) and np.all(out == 0)
+
+
+def test_hand_worked_two_key_example():
+    assert pins.pin_worked_example(os.path.join(GOLDEN, "two_key_worked_example.txt")) <= 1e-15
+
+
+def test_sampled_rows_equal_batch_rows():
+    from paper_2609_37626_amd import workloads as W
+    batch = W.make_custom([100, 260], H=4, q_chunk=3, seed=21)
+    args = (batch.q, batch.kv, batch.block_table, batch.seq_lens, 3, batch.softmax_scale)
+    out, lse = oracle.mla_attention(*args)
+    samples = [(0, 0, 1), (1, 2, 3), (1, 0, 0)]
+    so, sl = oracle.mla_attention_sampled(*args, samples=samples)
+    for k, (b, i, h) in enumerate(samples):
+        assert np.abs(so[k] - out[b * 3 + i, h]).max() <= 1e-13
+        assert abs(sl[k] - lse[b * 3 + i, h]) <= 1e-13
+
+
+# -------------------------------------------------- planted mistakes (CPU) ---
+
+_orig_rows = oracle.mla.attention_rows
+_orig_gather = oracle.mla.gather_history
+
+
+def _rows_mask_plus_one(Q, K, sigma, key_hi, key_lo=None, return_probs=False):
+    return _orig_rows(Q, K, sigma, np.minimum(np.asarray(key_hi) + 1, K.shape[0]), key_lo, return_probs)
+
+
+def _rows_mask_minus_one(Q, K, sigma, key_hi, key_lo=None, return_probs=False):
+    return _orig_rows(Q, K, sigma, np.maximum(np.asarray(key_hi) - 1, 1), key_lo, return_probs)
+
+
+def _rows_drop_rope(Q, K, sigma, key_hi, key_lo=None, return_probs=False):
+    Q = Q.copy()
+    Q[..., 512:] = 0
+    return _orig_rows(Q, K, sigma, key_hi, key_lo, return_probs)
+
+
+def _rows_value_from_tail(Q, K, sigma, key_hi, key_lo=None, return_probs=False):
+    res = list(_orig_rows(Q, np.concatenate([K[:, 64:], K[:, :64]], axis=1), sigma, key_hi,
+                          key_lo, return_probs))
+    Zonly = _orig_rows(Q, K, sigma, key_hi, key_lo, return_probs)
+    res[1] = Zonly[1]
+    return tuple(res)
+
+
+def _rows_scale_squared(Q, K, sigma, key_hi, key_lo=None, return_probs=False):
+    return _orig_rows(Q, K, sigma * sigma, key_hi, key_lo, return_probs)
+
+
+def _rows_lse_log2(Q, K, sigma, key_hi, key_lo=None, return_probs=False):
+    res = list(_orig_rows(Q, K, sigma, key_hi, key_lo, return_probs))
+    res[1] = res[1] / math.log(2.0)
+    return tuple(res)
+
+
+def _gather_reversed_in_page(kv, kv_scales, block_table, b, n_keys, kv_dtype):
+    j = np.arange(n_keys)
+    rows = block_table[b, j // 64].astype(np.int64) * 64 + (63 - j % 64)
+    flat = kv.reshape(-1, kv.shape[-1])[rows]
+    return oracle.formats.bf16_bits_to_f64(flat)
+
+
+def _gather_logical_as_physical(kv, kv_scales, block_table, b, n_keys, kv_dtype):
+    j = np.arange(n_keys)
+    flat = kv.reshape(-1, kv.shape[-1])[j]
+    return oracle.formats.bf16_bits_to_f64(flat)
+
+
+_orig_bf16 = oracle.formats.bf16_bits_to_f64
+
+
+def _bf16_bias_off(bits):
+    return _orig_bf16(bits) * 2.0
+
+
+_orig_e4m3 = oracle.formats.e4m3_bits_to_f64
+
+
+def _e4m3_fnuz_bias(bits):
+    return _orig_e4m3(bits) / 2.0
+
+
+_orig_merge = oracle.mla.merge_partials
+
+
+def _merge_flipped(parts_out, parts_lse):
+    parts_lse = np.asarray(parts_lse)
+    out, L = _orig_merge(parts_out, -parts_lse)
+    return out, -L
+
+
+MUTANTS = {
+    "causal limit one too far": ("attention_rows", _rows_mask_plus_one),
+    "causal limit one short": ("attention_rows", _rows_mask_minus_one),
+    "rope dims dropped from logits": ("attention_rows", _rows_drop_rope),
+    "value taken from the wrong 512 dims": ("attention_rows", _rows_value_from_tail),
+    "softmax scale squared": ("attention_rows", _rows_scale_squared),
+    "lse in log2": ("attention_rows", _rows_lse_log2),
+    "row order reversed inside a page": ("gather_history", _gather_reversed_in_page),
+    "block table ignored": ("gather_history", _gather_logical_as_physical),
+    "bf16 exponent bias off by one": ("bf16", _bf16_bias_off),
+    "e4m3 read as fnuz (bias 8)": ("e4m3", _e4m3_fnuz_bias),
+    "merge weights of wrong sign": ("merge_partials", _merge_flipped),
+}
+
+
+@contextlib.contextmanager
+def _planted(kind, fn):
+    targets = {
+        "attention_rows": [(oracle.mla, "attention_rows")],
+        "gather_history": [(oracle.mla, "gather_history")],
+        "bf16": [(oracle.mla, "bf16_bits_to_f64"), (oracle, "bf16_bits_to_f64")],
+        "e4m3": [(oracle.mla, "e4m3_bits_to_f64"), (oracle, "e4m3_bits_to_f64")],
+        "merge_partials": [(oracle.mla, "merge_partials"), (oracle, "merge_partials")],
+    }[kind]
+    saved = [(mod, name, getattr(mod, name)) for mod, name in targets]
+    try:
+        for mod, name in targets:
+            setattr(mod, name, fn)
+        yield
+    finally:
+        for mod, name, old in saved:
+            setattr(mod, name, old)
+
+
+def _pins_all_pass():
+    checks = [
+        (pins.pin_brute_force, TOL),
+        (pins.pin_sdpa, 1e-12),
+        (pins.pin_fp8_dequant, 1e-12),
+        (pins.pin_single_key, 0.0),
+        (pins.pin_zero_query, TOL),
+        (pins.pin_one_hot, TOL),
+        (pins.pin_chunk_rows_are_decodes, TOL),
+        (pins.pin_merge_identity, TOL),
+        (lambda: pins.pin_worked_example(os.path.join(GOLDEN, "two_key_worked_example.txt")), 1e-15),
+    ]
+    for fn, tol in checks:
+        try:
+            v = fn()
+        except Exception:
+            return False
+        if not (v <= tol):
+            return False
+    return True
+
+
+def test_pins_pass_on_unmodified_oracle():
+    assert _pins_all_pass()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name):
+    kind, fn = MUTANTS[name]
+    with _planted(kind, fn):
+        assert not _pins_all_pass(), f"no pin caught: {name}"
