@@ -92,18 +92,20 @@ typedef struct splash_mla_desc {
  * the passed ws_bytes provides: with too little room it splits less.
  * Layout (byte offsets from splash_mla_workspace_offsets, 256-byte aligned):
  *   [0] header int32[64]: [0] unit counter, [1] number of work units,
- *       [2] partial slots used, [3] pages per unit chosen, [4] debug status
+ *       [2] partial slots used, [3] pages per unit chosen, [4] debug status,
+ *       [5] drained workers, [6] number of split tiles, [7] total pages
  *   [1] work units int32[max_units][4] = {tile, first page, end page, slot},
  *       tile = b*q_chunk + i, slot = partial index or -1 (unit writes out/lse)
  *   [2] split offsets int32[B*q_chunk + 1] (partial slots of tile t are
  *       [off[t], off[t+1]); empty when the tile is a single unit)
- *   [3] partial lse fp32 [max_partials, H]
- *   [4] partial out fp32 [max_partials, H, 512]
+ *   [3] split tiles int32[B*q_chunk] (the tiles with partials, ascending)
+ *   [4] partial lse fp32 [max_partials, H]
+ *   [5] partial out fp32 [max_partials, H, 512]
  */
 #define SPLASH_DEFAULT_MAX_PARTIALS 1024
 size_t splash_mla_workspace_size(int32_t batch, int32_t q_chunk, int32_t num_heads,
                                  int32_t max_partials);
-/* Writes the five byte offsets above into offsets[5]; returns the total size. */
+/* Writes the six byte offsets above into offsets[6]; returns the total size. */
 size_t splash_mla_workspace_offsets(int32_t batch, int32_t q_chunk, int32_t num_heads,
                                     int32_t max_partials, size_t* offsets);
 
@@ -141,6 +143,22 @@ int splash_mla_run(const void* q, const void* kv_pages, const int32_t* block_tab
                    const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
                    const splash_mla_desc* desc, void* workspace, size_t ws_bytes,
                    void* stream);
+
+/*
+ * splash_mla_attend_units + splash_mla_combine_splits: splash_mla_run in its
+ * two launches.  attend_units processes every work unit of the plan: a tile
+ * (query row with all heads) that is one unit writes its out/lse rows
+ * directly; the units of a split tile write fp32 partials into the
+ * workspace.  combine_splits merges those partials into out/lse (its
+ * arguments must match the attend_units call).  Same argument rules as
+ * splash_mla_run.
+ */
+int splash_mla_attend_units(const void* q, const void* kv_pages, const int32_t* block_table,
+                            const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
+                            const splash_mla_desc* desc, void* workspace, size_t ws_bytes,
+                            void* stream);
+int splash_mla_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_desc* desc,
+                              void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * splash_mla_combine: merge partial attention results over disjoint key sets

@@ -1,0 +1,222 @@
+"""Thin ctypes binding of libsplash_attn (include/splash_attn.h).
+
+Argument marshalling only: every step of the attention path runs in the
+library's gfx950 kernels.  Tensors are torch tensors on the GPU; their device
+pointers and the current HIP stream are handed to the C entry points of the
+same names.  A missing library raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsplash_attn.so")
+
+SPLASH_OK = 0
+SPLASH_ERR_INVALID_ARGUMENT = -1
+SPLASH_ERR_UNSUPPORTED = -2
+SPLASH_ERR_MISALIGNED = -3
+SPLASH_ERR_WORKSPACE_TOO_SMALL = -4
+SPLASH_ERR_HIP = -5
+
+KV_BF16 = 0
+KV_FP8_E4M3 = 1
+FLAG_DEBUG_CHECK = 1
+FLAG_FORCE_SPLIT = 2
+DEFAULT_MAX_PARTIALS = 1024
+
+
+class SplashError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class MlaDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("num_heads", ctypes.c_int32),
+        ("dim_qk", ctypes.c_int32),
+        ("dim_v", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("max_pages_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("kv_scales", ctypes.c_void_p),
+        ("softmax_scale", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
+        ("split_pages", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+_VP = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+_PD = ctypes.POINTER(MlaDesc)
+_PI32 = ctypes.POINTER(ctypes.c_int32)
+
+_SIGNATURES = {
+    "splash_mla_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
+    "splash_mla_workspace_offsets": (_SZ, [_I32, _I32, _I32, _I32, ctypes.POINTER(_SZ)]),
+    "splash_mla_attend": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
+    "splash_mla_plan": (ctypes.c_int, [_VP, _I32, _PD, _VP, _SZ, _VP]),
+    "splash_mla_run": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
+    "splash_mla_attend_units": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
+    "splash_mla_combine_splits": (ctypes.c_int, [_I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
+    "splash_mla_combine": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP]),
+    "splash_mla_debug_gather": (ctypes.c_int, [_VP, _VP, _VP, _PD, _VP, _VP]),
+    "splash_mla_plan_host": (ctypes.c_int, [_PI32, _I32, _PD, _I32, _I32, _PI32, _I32, _PI32, _PI32]),
+    "splash_mla_max_units": (_I32, [_I32, _I32, _I32]),
+    "splash_device_workers": (_I32, []),
+    "splash_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "splash_last_error": (ctypes.c_char_p, []),
+    "splash_version": (ctypes.c_char_p, []),
+}
+
+
+def _hip_runtimes_mapped():
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({l.split()[-1] for l in f if "libamdhip64" in l})
+    except OSError:
+        return []
+
+
+def lib():
+    """Load libsplash_attn.so (built in-tree); raise if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_37626_amd.build`")
+    import torch  # noqa: F401  (load torch's HIP runtime first so the library binds to it)
+    handle = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(handle, name)
+        fn.restype = res
+        fn.argtypes = args
+    runtimes = _hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise RuntimeError(f"two HIP runtimes are mapped into this process: {runtimes}")
+    _lib = handle
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != SPLASH_OK:
+        L = lib()
+        raise SplashError(status, f"{L.splash_status_string(status).decode()}: {L.splash_last_error().decode()}")
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def make_desc(batch: int, num_heads: int, max_pages_per_seq: int, num_pages: int,
+              kv_dtype: int = KV_BF16, kv_scales=None, softmax_scale: float = 1.0 / 192 ** 0.5,
+              flags: int = 0, split_pages: int = 0) -> MlaDesc:
+    d = MlaDesc()
+    d.batch = batch
+    d.num_heads = num_heads
+    d.dim_qk = 576
+    d.dim_v = 512
+    d.page_size = 64
+    d.max_pages_per_seq = max_pages_per_seq
+    d.num_pages = num_pages
+    d.kv_dtype = kv_dtype
+    d.kv_scales = _ptr(kv_scales)
+    d.softmax_scale = float(np.float32(softmax_scale))
+    d.flags = flags
+    d.split_pages = split_pages
+    return d
+
+
+def workspace_size(batch: int, q_chunk: int, num_heads: int, max_partials: int = 0) -> int:
+    return int(lib().splash_mla_workspace_size(batch, q_chunk, num_heads, max_partials))
+
+
+def workspace_offsets(batch: int, q_chunk: int, num_heads: int, max_partials: int = 0):
+    offs = (_SZ * 6)()
+    total = lib().splash_mla_workspace_offsets(batch, q_chunk, num_heads, max_partials, offs)
+    return list(offs), int(total)
+
+
+def device_workers() -> int:
+    return int(lib().splash_device_workers())
+
+
+def splash_mla_attend(q, kv_pages, block_table, seq_lens, q_chunk: int, out, lse, desc: MlaDesc,
+                      workspace, stream=None) -> None:
+    _check(lib().splash_mla_attend(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
+                                   _ptr(out), _ptr(lse), ctypes.byref(desc), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_plan(seq_lens, q_chunk: int, desc: MlaDesc, workspace, stream=None) -> None:
+    _check(lib().splash_mla_plan(_ptr(seq_lens), q_chunk, ctypes.byref(desc), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_run(q, kv_pages, block_table, seq_lens, q_chunk: int, out, lse, desc: MlaDesc,
+                   workspace, stream=None) -> None:
+    _check(lib().splash_mla_run(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
+                                _ptr(out), _ptr(lse), ctypes.byref(desc), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_attend_units(q, kv_pages, block_table, seq_lens, q_chunk: int, out, lse, desc: MlaDesc,
+                            workspace, stream=None) -> None:
+    _check(lib().splash_mla_attend_units(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
+                                         _ptr(out), _ptr(lse), ctypes.byref(desc), _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_combine_splits(q_chunk: int, out, lse, desc: MlaDesc, workspace, stream=None) -> None:
+    _check(lib().splash_mla_combine_splits(q_chunk, _ptr(out), _ptr(lse), ctypes.byref(desc), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_combine(partials, partial_lse, split_indptr, batch: int, q_chunk: int, num_heads: int,
+                       out, out_lse=None, stream=None) -> None:
+    _check(lib().splash_mla_combine(_ptr(partials), _ptr(partial_lse), _ptr(split_indptr), batch, q_chunk,
+                                    num_heads, _ptr(out), _ptr(out_lse), _stream(stream)))
+
+
+def splash_mla_debug_gather(kv_pages, block_table, seq_lens, desc: MlaDesc, dense_out, stream=None) -> None:
+    _check(lib().splash_mla_debug_gather(_ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), ctypes.byref(desc),
+                                         _ptr(dense_out), _stream(stream)))
+
+
+def splash_mla_plan_host(seq_lens: np.ndarray, q_chunk: int, desc: MlaDesc, num_workers: int,
+                         max_partials: int = 0):
+    """Host mirror of the planner: returns (units [U,4], indptr [T+1], stats dict)."""
+    L = lib()
+    seq = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    T = int(seq.shape[0]) * q_chunk
+    max_units = int(L.splash_mla_max_units(int(seq.shape[0]), q_chunk, max_partials))
+    units = np.zeros((max(max_units, 1), 4), dtype=np.int32)
+    indptr = np.zeros(T + 1, dtype=np.int32)
+    stats = np.zeros(4, dtype=np.int32)
+    as_p = lambda a: a.ctypes.data_as(_PI32)
+    _check(L.splash_mla_plan_host(as_p(seq), q_chunk, ctypes.byref(desc), num_workers, max_partials,
+                                  as_p(units), max_units, as_p(indptr), as_p(stats)))
+    n = int(stats[0])
+    return units[:n].copy(), indptr, {"units": n, "partials": int(stats[1]), "chunk_pages": int(stats[2]),
+                                      "total_pages": int(stats[3])}
+
+
+def version() -> str:
+    return lib().splash_version().decode()

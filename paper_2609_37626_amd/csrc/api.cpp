@@ -1,0 +1,477 @@
+// C-ABI of libsplash_attn: argument validation, workspace layout, the host
+// mirror of the split planner, and the entry points declared in
+// include/splash_attn.h.  No C++ exception crosses this boundary.
+#include "splash_attn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <climits>
+#include <cstdarg>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "splash_common.hpp"
+
+using namespace splash;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SPLASH_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t off[6];  // header, units, indptr, split list, partial lse, partial out
+  size_t total;
+};
+
+Layout layout_for(int64_t T, int32_t H, int64_t max_partials) {
+  Layout L;
+  size_t o = 0;
+  L.off[0] = o; o = align_up(o + sizeof(int32_t) * kHeaderInts);
+  L.off[1] = o; o = align_up(o + 16 * (size_t)(T + max_partials));
+  L.off[2] = o; o = align_up(o + sizeof(int32_t) * (size_t)(T + 1));
+  L.off[3] = o; o = align_up(o + sizeof(int32_t) * (size_t)(T > 0 ? T : 1));
+  L.off[4] = o; o = align_up(o + sizeof(float) * (size_t)max_partials * H);
+  L.off[5] = o; o = align_up(o + sizeof(float) * (size_t)max_partials * H * kDimV);
+  L.total = o;
+  return L;
+}
+
+// Largest partial capacity that fits in ws_bytes.
+int64_t partials_for_bytes(int64_t T, int32_t H, size_t ws_bytes) {
+  const Layout base = layout_for(T, H, 0);
+  if (ws_bytes < base.total) return -1;
+  const size_t per = 16 + sizeof(float) * (size_t)H * (1 + kDimV);
+  int64_t mp = (int64_t)((ws_bytes - base.total) / per);
+  if (mp > INT32_MAX / 2) mp = INT32_MAX / 2;
+  while (mp > 0 && layout_for(T, H, mp).total > ws_bytes) --mp;
+  return mp;
+}
+
+Workspace workspace_view(void* ws, int64_t T, int32_t H, int64_t max_partials) {
+  const Layout L = layout_for(T, H, max_partials);
+  char* base = static_cast<char*>(ws);
+  Workspace w;
+  w.header = reinterpret_cast<int32_t*>(base + L.off[0]);
+  w.units = reinterpret_cast<int4*>(base + L.off[1]);
+  w.indptr = reinterpret_cast<int32_t*>(base + L.off[2]);
+  w.split_list = reinterpret_cast<int32_t*>(base + L.off[3]);
+  w.part_lse = reinterpret_cast<float*>(base + L.off[4]);
+  w.part_out = reinterpret_cast<float*>(base + L.off[5]);
+  w.max_units = (int32_t)(T + max_partials);
+  w.max_partials = (int32_t)max_partials;
+  return w;
+}
+
+// Partial slots that the 1024-page unit cap alone can force.
+int64_t forced_partials(int64_t T, int32_t max_pages_per_seq) {
+  if (max_pages_per_seq <= kMaxUnitPages) return 0;
+  return T * (int64_t)ceil_div(max_pages_per_seq, kMaxUnitPages);
+}
+
+int validate_desc(const splash_mla_desc* d, int32_t q_chunk) {
+  if (!d) return fail(SPLASH_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->batch < 0) return fail(SPLASH_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (q_chunk < 1) return fail(SPLASH_ERR_INVALID_ARGUMENT, "q_chunk must be >= 1 (got %d)", q_chunk);
+  if (d->dim_qk != kDimQK || d->dim_v != kDimV)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "dims must be qk=576, v=512 (got %d, %d)", d->dim_qk, d->dim_v);
+  if (d->page_size != kPage) return fail(SPLASH_ERR_UNSUPPORTED, "page_size must be 64 (got %d)", d->page_size);
+  if (d->num_heads < 16 || d->num_heads > kMaxHeads || d->num_heads % 16)
+    return fail(SPLASH_ERR_UNSUPPORTED, "num_heads must be a multiple of 16 in [16,128] (got %d)", d->num_heads);
+  if (d->kv_dtype != SPLASH_KV_BF16 && d->kv_dtype != SPLASH_KV_FP8_E4M3)
+    return fail(SPLASH_ERR_UNSUPPORTED, "unknown kv_dtype %d", d->kv_dtype);
+  if (d->kv_dtype == SPLASH_KV_FP8_E4M3 && !d->kv_scales)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "fp8 cache needs kv_scales");
+  if (!(std::isfinite(d->softmax_scale) && d->softmax_scale > 0.f))
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  if (d->max_pages_per_seq < 1 || d->num_pages < 1)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "max_pages_per_seq and num_pages must be >= 1");
+  if ((d->flags & SPLASH_FLAG_FORCE_SPLIT) && d->split_pages < 1)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "FORCE_SPLIT needs split_pages >= 1");
+  if ((int64_t)d->batch * q_chunk > INT32_MAX / 2)
+    return fail(SPLASH_ERR_UNSUPPORTED, "batch * q_chunk too large");
+  return SPLASH_OK;
+}
+
+std::atomic<int32_t> g_workers[64];
+
+int32_t device_workers() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
+  int32_t w = g_workers[dev].load(std::memory_order_relaxed);
+  if (w > 0) return w;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) return -1;
+  g_workers[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
+
+// Checks shared by plan / run / attend; fills the workspace view.
+int prepare(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* d, void* workspace,
+            size_t ws_bytes, Workspace* wv) {
+  if (!seq_lens) return fail(SPLASH_ERR_INVALID_ARGUMENT, "seq_lens is NULL");
+  if (!workspace) return fail(SPLASH_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SPLASH_ERR_MISALIGNED, "workspace not 16-byte aligned");
+  if (d->kv_dtype == SPLASH_KV_FP8_E4M3 && !aligned16(d->kv_scales))
+    return fail(SPLASH_ERR_MISALIGNED, "kv_scales not 16-byte aligned");
+  const int64_t T = (int64_t)d->batch * q_chunk;
+  const int64_t mp = partials_for_bytes(T, d->num_heads, ws_bytes);
+  if (mp < 0)
+    return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the minimum %zu", ws_bytes,
+                layout_for(T, d->num_heads, 0).total);
+  if (mp < forced_partials(T, d->max_pages_per_seq))
+    return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL,
+                "histories longer than %d pages must be split: need room for %lld partials, have %lld",
+                kMaxUnitPages, (long long)forced_partials(T, d->max_pages_per_seq), (long long)mp);
+  *wv = workspace_view(workspace, T, d->num_heads, mp);
+  return SPLASH_OK;
+}
+
+int check_device_data(const int32_t* block_table, const int32_t* seq_lens, int32_t q_chunk,
+                      const splash_mla_desc* d, const Workspace& wv, hipStream_t s) {
+  int32_t* res = wv.header + kHdrDebug;
+  hipError_t e = launch_check(block_table, seq_lens, d->batch, q_chunk, d->max_pages_per_seq, d->num_pages, res, s);
+  if (e != hipSuccess) return hip_fail(e, "check launch");
+  int32_t host = 0;
+  e = hipMemcpyAsync(&host, res, sizeof host, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "check readback");
+  if (host != INT32_MAX)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT,
+                "request %d: seq_len < q_chunk, history longer than the block-table row, or a block-table "
+                "entry outside [0, num_pages)",
+                host - 1);
+  return SPLASH_OK;
+}
+
+int do_plan(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* d, const Workspace& wv,
+            hipStream_t s) {
+  const int32_t G = device_workers();
+  if (G < 1) return fail(SPLASH_ERR_HIP, "cannot query the device's compute units");
+  PlanLaunch p;
+  p.seq_lens = seq_lens;
+  p.B = d->batch;
+  p.q_chunk = q_chunk;
+  p.G = G;
+  p.forced_chunk = (d->flags & SPLASH_FLAG_FORCE_SPLIT) ? d->split_pages : 0;
+  p.ws = wv;
+  hipError_t e = launch_plan(p, s);
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "plan launch");
+}
+
+int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens,
+                    int32_t q_chunk, void* out, float* lse, const splash_mla_desc* d, const Workspace& wv,
+                    hipStream_t s) {
+  const int32_t G = device_workers();
+  if (G < 1) return fail(SPLASH_ERR_HIP, "cannot query the device's compute units");
+  AttendLaunch a;
+  a.q = q;
+  a.kv = kv_pages;
+  a.kv_scales = d->kv_scales;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.out = out;
+  a.lse = lse;
+  a.bt_stride = d->max_pages_per_seq;
+  a.q_chunk = q_chunk;
+  a.H = d->num_heads;
+  a.kv_dtype = d->kv_dtype;
+  a.B = d->batch;
+  a.softmax_scale = d->softmax_scale;
+  a.ws = wv;
+  hipError_t e = launch_attend(a, G, s);
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "attend launch");
+}
+
+int do_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_desc* d, const Workspace& wv,
+                      hipStream_t s) {
+  CombineLaunch c;
+  c.partials = wv.part_out;
+  c.partial_lse = wv.part_lse;
+  c.indptr = wv.indptr;
+  c.item_list = wv.split_list;
+  c.item_count = wv.header + kHdrSplitTiles;
+  c.B = d->batch * q_chunk;
+  c.q_chunk = 1;
+  c.H = d->num_heads;
+  c.out = out;
+  c.out_lse = lse;
+  c.write_empty = false;
+  hipError_t e = launch_combine(c, s);
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "combine launch");
+}
+
+int do_run(const void* q, const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens,
+           int32_t q_chunk, void* out, float* lse, const splash_mla_desc* d, const Workspace& wv, hipStream_t s) {
+  int st = do_attend_units(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, d, wv, s);
+  if (st != SPLASH_OK) return st;
+  return do_combine_splits(q_chunk, out, lse, d, wv, s);
+}
+
+int check_tensors(const void* q, const void* kv_pages, const int32_t* block_table, void* out, const float* lse) {
+  if (!q || !kv_pages || !block_table || !out)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "q, kv_pages, block_table and out must be non-NULL");
+  if (!aligned16(q) || !aligned16(kv_pages) || !aligned16(out))
+    return fail(SPLASH_ERR_MISALIGNED, "q, kv_pages and out must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(block_table) & 3u) || (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(SPLASH_ERR_MISALIGNED, "block_table and lse must be 4-byte aligned");
+  return SPLASH_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t splash_mla_workspace_size(int32_t batch, int32_t q_chunk, int32_t num_heads, int32_t max_partials) {
+  if (batch < 0 || q_chunk < 1 || num_heads < 1) return 0;
+  if (max_partials <= 0) max_partials = SPLASH_DEFAULT_MAX_PARTIALS;
+  return layout_for((int64_t)batch * q_chunk, num_heads, max_partials).total;
+}
+
+size_t splash_mla_workspace_offsets(int32_t batch, int32_t q_chunk, int32_t num_heads, int32_t max_partials,
+                                    size_t* offsets) {
+  if (batch < 0 || q_chunk < 1 || num_heads < 1) return 0;
+  if (max_partials <= 0) max_partials = SPLASH_DEFAULT_MAX_PARTIALS;
+  const Layout L = layout_for((int64_t)batch * q_chunk, num_heads, max_partials);
+  if (offsets)
+    for (int k = 0; k < 6; ++k) offsets[k] = L.off[k];
+  return L.total;
+}
+
+int32_t splash_mla_max_units(int32_t batch, int32_t q_chunk, int32_t max_partials) {
+  if (max_partials <= 0) max_partials = SPLASH_DEFAULT_MAX_PARTIALS;
+  return (int32_t)((int64_t)batch * q_chunk + max_partials);
+}
+
+int32_t splash_device_workers(void) {
+  const int32_t w = device_workers();
+  return w < 1 ? 1 : w;
+}
+
+int splash_mla_plan(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* desc, void* workspace,
+                    size_t ws_bytes, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  Workspace wv;
+  if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
+  return do_plan(seq_lens, q_chunk, desc, wv, static_cast<hipStream_t>(stream));
+}
+
+int splash_mla_run(const void* q, const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens,
+                   int32_t q_chunk, void* out, float* lse, const splash_mla_desc* desc, void* workspace,
+                   size_t ws_bytes, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if ((st = check_tensors(q, kv_pages, block_table, out, lse)) != SPLASH_OK) return st;
+  Workspace wv;
+  if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
+    if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
+  return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
+}
+
+int splash_mla_attend_units(const void* q, const void* kv_pages, const int32_t* block_table,
+                            const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
+                            const splash_mla_desc* desc, void* workspace, size_t ws_bytes, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if ((st = check_tensors(q, kv_pages, block_table, out, lse)) != SPLASH_OK) return st;
+  Workspace wv;
+  if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
+  return do_attend_units(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv,
+                         static_cast<hipStream_t>(stream));
+}
+
+int splash_mla_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_desc* desc,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if (!out) return fail(SPLASH_ERR_INVALID_ARGUMENT, "out is NULL");
+  if (!aligned16(out)) return fail(SPLASH_ERR_MISALIGNED, "out must be 16-byte aligned");
+  if (!workspace) return fail(SPLASH_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SPLASH_ERR_MISALIGNED, "workspace not 16-byte aligned");
+  const int64_t T = (int64_t)desc->batch * q_chunk;
+  const int64_t mp = partials_for_bytes(T, desc->num_heads, ws_bytes);
+  if (mp < 0) return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+  const Workspace wv = workspace_view(workspace, T, desc->num_heads, mp);
+  return do_combine_splits(q_chunk, out, lse, desc, wv, static_cast<hipStream_t>(stream));
+}
+
+int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens,
+                      int32_t q_chunk, void* out, float* lse, const splash_mla_desc* desc, void* workspace,
+                      size_t ws_bytes, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if ((st = check_tensors(q, kv_pages, block_table, out, lse)) != SPLASH_OK) return st;
+  Workspace wv;
+  if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
+    if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
+  if ((st = do_plan(seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
+  return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
+}
+
+int splash_mla_combine(const float* partials, const float* partial_lse, const int32_t* split_indptr, int32_t batch,
+                       int32_t q_chunk, int32_t num_heads, void* out, float* out_lse, void* stream) {
+  if (batch < 0 || q_chunk < 1 || num_heads < 1)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "batch >= 0, q_chunk >= 1 and num_heads >= 1 required");
+  if (batch == 0) return SPLASH_OK;
+  if (!partials || !partial_lse || !split_indptr || !out)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "partials, partial_lse, split_indptr and out must be non-NULL");
+  if (!aligned16(partials) || !aligned16(out))
+    return fail(SPLASH_ERR_MISALIGNED, "partials and out must be 16-byte aligned");
+  CombineLaunch c;
+  c.partials = partials;
+  c.partial_lse = partial_lse;
+  c.indptr = split_indptr;
+  c.item_list = nullptr;
+  c.item_count = nullptr;
+  c.B = batch;
+  c.q_chunk = q_chunk;
+  c.H = num_heads;
+  c.out = out;
+  c.out_lse = out_lse;
+  c.write_empty = true;
+  hipError_t e = launch_combine(c, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "combine launch");
+}
+
+int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens,
+                            const splash_mla_desc* desc, void* dense_out, void* stream) {
+  int st = validate_desc(desc, 1);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if (!kv_pages || !block_table || !seq_lens || !dense_out)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "kv_pages, block_table, seq_lens and dense_out must be non-NULL");
+  if (!aligned16(kv_pages) || !aligned16(dense_out))
+    return fail(SPLASH_ERR_MISALIGNED, "kv_pages and dense_out must be 16-byte aligned");
+  const int32_t row_bytes = desc->kv_dtype == SPLASH_KV_FP8_E4M3 ? kDimQK : 2 * kDimQK;
+  hipError_t e = launch_gather(kv_pages, block_table, seq_lens, desc->batch, desc->max_pages_per_seq, row_bytes,
+                               dense_out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "gather launch");
+}
+
+int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const splash_mla_desc* desc,
+                         int32_t num_workers, int32_t max_partials, int32_t* units_out, int32_t max_units,
+                         int32_t* indptr_out, int32_t* stats_out) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (num_workers < 1) return fail(SPLASH_ERR_INVALID_ARGUMENT, "num_workers must be >= 1");
+  const int32_t B = desc->batch, T = B * q_chunk;
+  if (B > 0 && (!seq_lens_host || !units_out || !indptr_out || !stats_out))
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "NULL host buffer");
+  if (max_partials <= 0) max_partials = SPLASH_DEFAULT_MAX_PARTIALS;
+  auto pages = [&](int32_t t) {
+    const int32_t b = t / q_chunk, i = t - b * q_chunk;
+    const int32_t L = tile_keys(seq_lens_host[b], q_chunk, i);
+    return L > 0 ? ceil_div(L, kPage) : 0;
+  };
+  int64_t total = 0;
+  int32_t mx = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    total += pages(t);
+    mx = std::max(mx, pages(t));
+  }
+  const int32_t max_pages = mx > 0 ? mx : 1;
+  const int32_t cap_units = std::min<int64_t>(max_units, (int64_t)T + max_partials);
+  auto evaluate = [&](int32_t c, int64_t* cost) {
+    int64_t W = 0, S = 0;
+    for (int32_t t = 0; t < T; ++t) {
+      const int32_t P = pages(t), n = P > 0 ? ceil_div(P, c) : 0;
+      W += n;
+      S += n > 1 ? n : 0;
+    }
+    const bool ok = S <= max_partials && W <= (int64_t)T + max_partials;
+    *cost = ok ? plan_cost(c, W, S, total, max_pages, num_workers, kPlanCosts) : INT64_MAX;
+  };
+  int32_t best_c = 0;
+  int64_t best = INT64_MAX;
+  for (int k = 0; k < kNumCandidates; ++k) {
+    const int32_t c = plan_candidate(k, max_pages);
+    int64_t cost;
+    evaluate(c, &cost);
+    if (k == 0 || cost < best) {
+      best = cost;
+      best_c = c;
+    }
+  }
+  if (desc->flags & SPLASH_FLAG_FORCE_SPLIT) {
+    const int32_t c = std::min(desc->split_pages, (int32_t)kMaxUnitPages);
+    int64_t cost;
+    evaluate(c, &cost);
+    if (cost != INT64_MAX) best_c = c;
+  }
+  const int32_t c = best_c;
+  int32_t nu = 0, ns = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    const int32_t P = pages(t), n = P > 0 ? ceil_div(P, c) : 0;
+    indptr_out[t] = ns;
+    for (int32_t u = 0; u < n; ++u) {
+      if (nu >= cap_units) return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "more units than max_units");
+      int32_t* r = units_out + 4 * (size_t)nu++;
+      r[0] = t;
+      r[1] = unit_begin(P, n, u);
+      r[2] = unit_begin(P, n, u + 1);
+      r[3] = n > 1 ? ns + u : -1;
+    }
+    ns += n > 1 ? n : 0;
+  }
+  if (T >= 0 && indptr_out) indptr_out[T] = ns;
+  if (stats_out) {
+    stats_out[0] = nu;
+    stats_out[1] = ns;
+    stats_out[2] = c;
+    stats_out[3] = total > INT32_MAX ? INT32_MAX : (int32_t)total;
+  }
+  return SPLASH_OK;
+}
+
+const char* splash_status_string(int status) {
+  switch (status) {
+    case SPLASH_OK: return "ok";
+    case SPLASH_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case SPLASH_ERR_UNSUPPORTED: return "unsupported";
+    case SPLASH_ERR_MISALIGNED: return "misaligned pointer";
+    case SPLASH_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case SPLASH_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* splash_last_error(void) { return g_last_error.c_str(); }
+
+const char* splash_version(void) { return "libsplash_attn 0.1.0 (gfx950)"; }
+
+}  // extern "C"

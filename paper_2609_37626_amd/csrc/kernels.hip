@@ -1,0 +1,817 @@
+// gfx950 kernels of libsplash_attn: split planner, paged MLA attend, LSE
+// combine, page gather and device-data check.
+//
+// Attend kernel design (one persistent workgroup per compute unit):
+//  * Work unit = (query row n with all H heads, page range).  Units come from
+//    a device queue filled by the planner; workers draw them with one atomic.
+//  * 4 waves; wave w owns heads [32w, 32w+32).  Its 32 query rows stay in
+//    VGPRs for the whole unit (36 x 16-byte MFMA B fragments).
+//  * KV is staged 32 rows (half a page, one "step") at a time straight from
+//    HBM into LDS with 16-byte direct-to-LDS loads, 3 steps in flight in a
+//    4-deep ring.  The chunk order of each row is XOR-permuted by row so the
+//    operand reads below spread over the LDS banks.
+//  * S^T[32 keys x 32 heads] = K Q^T on v_mfma_f32_32x32x16_bf16 (36 MFMAs),
+//    K read from LDS as the A operand.  In that C layout a lane holds one head
+//    and 16 keys, so the row max needs one cross-half exchange.
+//  * Online softmax in base 2 with lazy rescaling: the running max only moves
+//    (and O is only rescaled) when the new max exceeds it by more than 8, so
+//    P <= 2^8; the result is exact because numerator and denominator share
+//    the same reference max.
+//  * O^T[512 x 32 heads] += V^T P^T on MFMA: P^T comes straight from the S^T
+//    registers (the key order of the contraction is permuted to match the C
+//    layout) and V^T is read from the same staged rows with ds_read_b64_tr_b16
+//    (bf16) or ds_read_b64_tr_b8 (fp8) transposing loads.  O lives in 256
+//    accumulation registers per lane.
+//  * fp8 cache: E4M3 codes convert exactly to bf16; the per-token scale is
+//    applied in fp32 to the score and to P before P is rounded for PV.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "kernels.hpp"
+#include "splash_common.hpp"
+
+namespace splash {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+#define LDS_AS __attribute__((address_space(3)))
+
+// s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt[3:0], [15:14]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier that does not drain outstanding global->LDS loads (a
+// __syncthreads() would wait for every in-flight load).  LDS writes of this
+// wave are completed first; the compiler may not move memory accesses across.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt((0x3F & 15) | (7 << 4) | (0 << 8) | ((0x3F >> 4) << 14));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Opaque copy: keeps the compiler from hoisting work derived from v out of a loop.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+__device__ __forceinline__ unsigned pack_bf16x2(float a, float b) {
+  bf16x2 v = __builtin_convertvector((f32x2){a, b}, bf16x2);
+  return __builtin_bit_cast(unsigned, v);
+}
+
+// 8 E4M3 codes (two dwords) -> 8 bf16 (exact).
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 raw) {
+  u32x4 r;
+  r[0] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[0], 1.0f, false));
+  r[1] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[0], 1.0f, true));
+  r[2] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[1], 1.0f, false));
+  r[3] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[1], 1.0f, true));
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+__device__ __forceinline__ float wave_xor32(float v) { return __shfl_xor(v, 32, 64); }
+
+// ============================================================== planner ===
+
+__device__ __forceinline__ int32_t dev_tile_pages(const int32_t* seq_lens, int32_t q_chunk, int32_t t) {
+  int32_t b = t / q_chunk, i = t - b * q_chunk;
+  int32_t L = tile_keys(seq_lens[b], q_chunk, i);
+  return L > 0 ? ceil_div(L, kPage) : 0;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_max(T v) {
+  for (int o = 32; o > 0; o >>= 1) {
+    T w = __shfl_xor(v, o, 64);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// Exclusive block scan of one int per thread (1024 threads); returns the
+// exclusive prefix and writes the block total to *total.
+__device__ int32_t block_exclusive_scan(int32_t v, int32_t* wave_buf, int32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int32_t inc = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    int32_t n = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += n;
+  }
+  if (lane == 63) wave_buf[wave] = inc;
+  __syncthreads();
+  if (wave == 0) {
+    const int32_t x = lane < 16 ? wave_buf[lane] : 0;
+    int32_t run = x;
+    for (int o = 1; o < 16; o <<= 1) {
+      const int32_t n = __shfl_up(run, o, 64);
+      if (lane >= o) run += n;
+    }
+    if (lane < 16) wave_buf[lane] = run - x;
+    if (lane == 15) wave_buf[16] = run;
+  }
+  __syncthreads();
+  int32_t res = wave_buf[wave] + inc - v;
+  *total = wave_buf[16];
+  __syncthreads();
+  return res;
+}
+
+constexpr int kPlanLdsTiles = 8192;  // tile page counts cached in LDS up to this many tiles
+
+__global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
+  __shared__ int32_t s_pages[kPlanLdsTiles];
+  __shared__ int64_t s_red64[16];
+  __shared__ int32_t s_red32[16];
+  __shared__ int64_t s_cost[kNumCandidates + 1];
+  __shared__ int32_t s_cand[kNumCandidates + 1];
+  __shared__ int32_t s_scan[17];
+  __shared__ int32_t s_chunk;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int32_t T = p.B * p.q_chunk;
+  const bool cached = T <= kPlanLdsTiles;
+  int32_t* hdr = p.ws.header;
+  auto pages_of = [&](int32_t t) -> int32_t {
+    return cached ? s_pages[t] : dev_tile_pages(p.seq_lens, p.q_chunk, t);
+  };
+
+  // 1. page counts (cached), total and largest tile.
+  int64_t tot = 0;
+  int32_t mx = 0;
+  for (int32_t t = tid; t < T; t += 1024) {
+    const int32_t P = dev_tile_pages(p.seq_lens, p.q_chunk, t);
+    if (cached) s_pages[t] = P;
+    tot += P;
+    mx = P > mx ? P : mx;
+  }
+  tot = wave_sum(tot);
+  mx = wave_max(mx);
+  if (lane == 0) { s_red64[wave] = tot; s_red32[wave] = mx; }
+  __syncthreads();
+  tot = 0; mx = 0;
+  for (int w = 0; w < 16; ++w) { tot += s_red64[w]; mx = s_red32[w] > mx ? s_red32[w] : mx; }
+  const int64_t total_pages = tot;
+  const int32_t max_pages = mx > 0 ? mx : 1;
+
+  // 2. unit size: evaluate every candidate (and a forced size), take the argmin.
+  for (int k = wave; k <= kNumCandidates; k += 16) {
+    int32_t c;
+    if (k < kNumCandidates) {
+      c = plan_candidate(k, max_pages);
+    } else {
+      if (p.forced_chunk <= 0) { if (lane == 0) { s_cost[k] = INT64_MAX; s_cand[k] = 0; } continue; }
+      c = p.forced_chunk < kMaxUnitPages ? p.forced_chunk : kMaxUnitPages;
+    }
+    int64_t W = 0, S = 0;
+    for (int32_t t = lane; t < T; t += 64) {
+      const int32_t P = pages_of(t);
+      const int32_t n = P > 0 ? ceil_div(P, c) : 0;
+      W += n;
+      S += n > 1 ? n : 0;
+    }
+    W = wave_sum(W);
+    S = wave_sum(S);
+    if (lane == 0) {
+      const bool ok = S <= p.ws.max_partials && W <= p.ws.max_units;
+      s_cost[k] = ok ? plan_cost(c, W, S, total_pages, max_pages, p.G, kPlanCosts) : INT64_MAX;
+      s_cand[k] = c;
+    }
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // first minimum over the candidates (smallest index on ties)
+    int64_t best = INT64_MAX;
+    int bk = kNumCandidates;
+    for (int k = lane; k < kNumCandidates; k += 64)
+      if (s_cost[k] < best) { best = s_cost[k]; bk = k; }
+    for (int o = 32; o > 0; o >>= 1) {
+      const int64_t ob = __shfl_xor(best, o, 64);
+      const int ok = __shfl_xor(bk, o, 64);
+      if (ob < best || (ob == best && ok < bk)) { best = ob; bk = ok; }
+    }
+    if (lane == 0) {
+      if (bk >= kNumCandidates) bk = 0;
+      if (p.forced_chunk > 0 && s_cost[kNumCandidates] != INT64_MAX) bk = kNumCandidates;
+      s_chunk = s_cand[bk];
+    }
+  }
+  __syncthreads();
+  const int32_t c = s_chunk;
+
+  // 3. scan units / partial slots / split tiles over the tiles, write the list.
+  int32_t carry_u = 0, carry_s = 0, carry_f = 0;
+  for (int32_t base = 0; base < T; base += 1024) {
+    const int32_t t = base + tid;
+    const int32_t P = t < T ? pages_of(t) : 0;
+    const int32_t n = P > 0 ? ceil_div(P, c) : 0;
+    const int32_t sp = n > 1 ? n : 0;
+    const int32_t f = n > 1 ? 1 : 0;
+    int32_t tu, ts, tf;
+    const int32_t eu = block_exclusive_scan(n, s_scan, &tu) + carry_u;
+    const int32_t es = block_exclusive_scan(sp, s_scan, &ts) + carry_s;
+    const int32_t ef = block_exclusive_scan(f, s_scan, &tf) + carry_f;
+    if (t < T) {
+      for (int32_t u = 0; u < n && eu + u < p.ws.max_units; ++u) {
+        int4 rec;
+        rec.x = t;
+        rec.y = unit_begin(P, n, u);
+        rec.z = unit_begin(P, n, u + 1);
+        rec.w = n > 1 ? es + u : -1;
+        p.ws.units[eu + u] = rec;
+      }
+      p.ws.indptr[t] = es < p.ws.max_partials ? es : p.ws.max_partials;
+      if (f) p.ws.split_list[ef] = t;
+    }
+    carry_u += tu;
+    carry_s += ts;
+    carry_f += tf;
+  }
+  if (tid == 0) {
+    p.ws.indptr[T] = carry_s;
+    hdr[kHdrGrab] = 0;
+    hdr[kHdrDone] = 0;
+    hdr[kHdrUnits] = carry_u < p.ws.max_units ? carry_u : p.ws.max_units;
+    hdr[kHdrPartials] = carry_s;
+    hdr[kHdrChunk] = c;
+    hdr[kHdrSplitTiles] = carry_f;
+    hdr[kHdrTotalPages] = total_pages > INT32_MAX ? INT32_MAX : (int32_t)total_pages;
+  }
+}
+
+// =============================================================== attend ===
+//
+// LDS layout of one staged step (32 cache rows): chunk-major.  A row is 72
+// (bf16) or 36 (fp8) 16-byte chunks; chunk c of row r sits at byte
+//   c * 512 + (r ^ swz(c)) * 16,   swz(c) = 4*(c & 1) ^ 8*((c >> 1) & 1).
+// Each 1 KB direct-to-LDS load instruction then fills chunks 2s, 2s+1 of all
+// 32 rows, every operand read below is a lane-dependent base plus an
+// immediate, and the row XOR keeps the transposing reads conflict-free.
+
+template <bool FP8>
+struct StepLayout {
+  static constexpr int kRowBytes = FP8 ? kDimQK : 2 * kDimQK;       // 576 / 1152
+  static constexpr int kChunks = kRowBytes / 16;                     // 36 / 72
+  static constexpr int kData = kStepKeys * kRowBytes;                // 18432 / 36864
+  static constexpr int kBuf = FP8 ? kData + 256 : kData;             // + fp32 scales
+  static constexpr int kBufs = 4;
+  static constexpr int kSegs = kChunks / 2;                          // 1 KB segments: 18 / 36
+  static constexpr int kLoadsPerStep = FP8 ? 5 : 9;                  // per wave
+};
+
+// Direct global->LDS loads, issued through asm so that the compiler's wait
+// insertion (which cannot tell which LDS bytes they write) does not drain
+// them before every LDS read; the kernel waits for them explicitly.  The
+// LDS destination is M0 + 16 * lane (4 * lane for the dword form); M0 is
+// restored afterwards.
+__device__ __forceinline__ void dma_b128(const void* gptr, const uint8_t LDS_AS* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gptr), "s"(m0)
+      : "memory");
+}
+__device__ __forceinline__ void dma_b32(const void* gptr, const uint8_t LDS_AS* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gptr), "s"(m0)
+      : "memory");
+}
+
+__device__ __forceinline__ uint32_t chunk_swz(uint32_t c) { return 4u * (c & 1u) ^ 8u * ((c >> 1) & 1u); }
+
+// Issue the direct-to-LDS loads of one step.  Wave w fills segments
+// s = 4t + w; lane l writes row slot (l & 31) of chunk 2s + (l >> 5), which
+// holds logical row (l & 31) ^ swz(chunk).  src_lane is the lane's byte
+// offset inside the step for t = 0 (see attend_kernel).
+template <bool FP8>
+__device__ __forceinline__ void issue_step(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
+                                           uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
+  using L = StepLayout<FP8>;
+#pragma unroll
+  for (int t = 0; t < L::kLoadsPerStep; ++t) {
+    const int seg = 4 * t + wave;
+    if (!FP8 || t < 4 || seg < L::kSegs) {
+      dma_b128(step_src + src_lane + 128 * t, buf + 4096 * t + 1024 * wave);
+    } else {
+      // waves 2 and 3: the step's 32 per-token scales (lanes 32..63 repeat
+      // them; both waves write identical bytes to the same place).
+      const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+      dma_b32(step_scales + (lane & 31), buf + L::kData);
+    }
+  }
+}
+
+// QK^T MFMAs are issued through inline asm with a VGPR accumulator: the
+// compiler picks one MFMA destination class per function, and the output
+// accumulator already fills the 256 accumulation registers.  Two independent
+// chains alternate so no MFMA reads a result still in flight; wait_mfma_vgpr()
+// covers the latency before VALU code reads the chains.
+template <bool FIRST, bool VALU_SRC>
+__device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  if constexpr (FIRST) {
+    if constexpr (VALU_SRC)
+      asm volatile("s_nop 2\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(a), "v"(b));
+    else
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(acc) : "v"(a), "v"(b));
+  } else {
+    if constexpr (VALU_SRC)
+      asm volatile("s_nop 2\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+    else
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+  }
+}
+
+__device__ __forceinline__ void wait_mfma_vgpr(f32x16& a0, f32x16& a1) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a0), "+v"(a1));
+}
+
+// K operand fragment ks (A operand: lane = key row n32, 8 dims).
+template <bool FP8>
+__device__ __forceinline__ bf16x8 load_k_frag(const uint8_t LDS_AS* buf, const uint32_t* kbase, int ks) {
+  if constexpr (!FP8) {
+    // chunk 2ks + h; base chosen by ks parity
+    return *(const bf16x8 LDS_AS*)(buf + kbase[ks & 1] + 1024 * ks);
+  } else {
+    // chunk ks, half h; base chosen by ks & 3
+    const u32x2 raw = *(const u32x2 LDS_AS*)(buf + kbase[ks & 3] + 2048 * (ks >> 2));
+    return fp8x8_to_bf16(raw);
+  }
+}
+
+// V^T operand fragment (column block cb, key half kh) via transposing reads.
+template <bool FP8>
+__device__ __forceinline__ bf16x8 load_v_frag(const uint8_t LDS_AS* buf, const uint32_t* vbase, int cb, int kh) {
+  if constexpr (!FP8) {
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 LDS_AS*)(buf + vbase[0] + 2048 * cb + 256 * kh));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 LDS_AS*)(buf + vbase[1] + 2048 * cb + 256 * kh));
+    const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, (u32x4){l2[0], l2[1], h2[0], h2[1]});
+  } else {
+    const i32x2 raw =
+        __builtin_amdgcn_ds_read_tr8_b64_v2i32((i32x2 LDS_AS*)(buf + vbase[cb & 1] + 2048 * (cb >> 1) + 256 * kh));
+    return fp8x8_to_bf16(__builtin_bit_cast(u32x2, raw));
+  }
+}
+
+template <bool FP8>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void attend_kernel(AttendLaunch a) {
+  using L = StepLayout<FP8>;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBufs * L::kBuf];
+  __shared__ int32_t s_bt[kMaxUnitPages];
+  __shared__ int4 s_unit;
+  __shared__ int32_t s_restart;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
+  const int h = lane >> 5, n32 = lane & 31;
+  const int head = wave * 32 + n32;
+  const bool head_ok = head < a.H;
+  const bool wave_active = wave * 32 < a.H;
+  const int32_t num_units = a.ws.header[kHdrUnits];
+  if (tid == 0) s_restart = 0;
+  const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
+  const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
+  uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
+
+  // ---- per-lane LDS / global offsets (bytes), fixed for the kernel ----
+  // DMA: segment s = 4t + wave holds chunk c = 2s + h, row slot n32, i.e.
+  // logical row n32 ^ swz(c) with swz(c) = 4h ^ 8*(wave & 1).
+  const uint32_t dma_row = n32 ^ (4u * h) ^ (8u * (wave & 1));
+  const uint32_t src_lane = dma_row * L::kRowBytes + (2 * wave + h) * 16;
+  // Row this lane's DMA slots hold (for zeroing rows past the history end).
+  const uint32_t dma_slot = 1024 * wave + 16 * lane;
+  // K operand.
+  uint32_t kbase[4];
+  if constexpr (!FP8) {
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+      const uint32_t c = 2 * par + h;                 // chunk 2ks + h, ks even/odd
+      kbase[par] = h * 512 + (n32 ^ chunk_swz(c)) * 16 + 0 * c;
+    }
+    kbase[2] = kbase[3] = 0;
+  } else {
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) kbase[r4] = r4 * 512 + (n32 ^ chunk_swz(r4)) * 16 + 8 * h;
+  }
+  // V operand.
+  const int i16 = lane & 15, g = lane >> 4;
+  uint32_t vbase[2];
+  if constexpr (!FP8) {
+    // tr16: source lane supplies row 16kh + 8t + 4h + (i16>>2), columns
+    // 32cb + 16(g&1) + 4(i16&3) .. +4, i.e. chunk 4cb + cc, 8*(i16&1) bytes in.
+    const uint32_t cc = 2 * (g & 1) + ((i16 >> 1) & 1);
+    const uint32_t sw = chunk_swz(cc);                  // swz(4cb + cc) = swz(cc)
+    const uint32_t rb = 4 * h + (i16 >> 2);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) vbase[t] = cc * 512 + ((8 * t + rb) ^ sw) * 16 + 8 * (i16 & 1);
+  } else {
+    // tr8: source lane s supplies key k = s>>1 of the slot order (rows
+    // 8(k>>2) + 4h + (k&3)), 8 bytes of chunk 2cb + (g&1).
+    const int k = i16 >> 1;
+    const uint32_t rowk = 8 * (k >> 2) + 4 * h + (k & 3);
+#pragma unroll
+    for (int cbp = 0; cbp < 2; ++cbp) {
+      const uint32_t c = 2 * cbp + (g & 1);
+      vbase[cbp] = c * 512 + (rowk ^ chunk_swz(c)) * 16 + 8 * (i16 & 1);
+    }
+  }
+
+  for (;;) {
+    if (tid == 0) {
+      int32_t u = atomicAdd(&a.ws.header[kHdrGrab], 1);
+      s_unit = u < num_units ? a.ws.units[u] : make_int4(-1, 0, 0, 0);
+    }
+    __syncthreads();
+    const int4 unit = s_unit;
+    if (unit.x < 0) break;
+    const int tile = unit.x, p0 = unit.y, p1 = unit.z, slot = unit.w;
+    // The explicit vmcnt waits below assume every older memory operation of
+    // this wave has completed (stores may complete out of order with loads).
+    wait_vmcnt<0>();
+    const int b = tile / a.q_chunk, qi = tile - b * a.q_chunk;
+    const int Lk = tile_keys(a.seq_lens[b], a.q_chunk, qi);
+    const int key_begin = p0 * kPage;
+    const int key_end = min(p1 * kPage, Lk);
+    const int nsteps = (key_end - key_begin + kStepKeys - 1) / kStepKeys;
+
+    const int32_t* bt = a.block_table + (size_t)b * a.bt_stride + p0;
+    for (int k = tid; k < p1 - p0; k += 256) s_bt[k] = bt[k];
+
+    // Query fragment: B operand, row = head, k = dims 16*ks + 8*h + [0, 8).
+    bf16x8 qf[36];
+    {
+      const int qhead = head_ok ? head : 0;  // in-bounds row for padding heads
+      const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)tile * a.H + qhead) * kDimQK + 8 * h;
+#pragma unroll
+      for (int ks = 0; ks < 36; ++ks) {
+        u32x4 v = *(const u32x4*)(qrow + 16 * ks);
+        if (!head_ok) v = (u32x4){0, 0, 0, 0};
+        qf[ks] = __builtin_bit_cast(bf16x8, v);
+      }
+    }
+    __syncthreads();  // block-table slice visible
+
+    auto step_src = [&](int j) {
+      const int key = key_begin + j * kStepKeys;
+      const int phys = s_bt[(key >> 6) - p0];
+      return kv + (size_t)phys * (kPage * L::kRowBytes) + (size_t)((key >> 5) & 1) * L::kData;
+    };
+    auto step_scales = [&](int j) -> const float* {
+      if constexpr (!FP8) return nullptr;
+      const int key = key_begin + j * kStepKeys;
+      const int phys = s_bt[(key >> 6) - p0];
+      return a.kv_scales + (size_t)phys * kPage + ((key >> 5) & 1) * kStepKeys;
+    };
+    // Softmax reference: fixed at the first step's max (O is still zero
+    // there), never moved afterwards, so O is never rescaled inside the loop.
+    // If a later logit exceeds it by more than 64 (base 2), P could overflow:
+    // the workgroup then redoes the unit with the unit's true max, which is
+    // known after the first pass.
+    float m_init = -INFINITY;
+    f32x16 o[16];
+    float m_ref, l_run, l_exact;
+    for (;;) {
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+      if (j < nsteps) issue_step<FP8>(step_src(j), step_scales(j), src_lane, sm + j * L::kBuf, wave);
+
+#pragma unroll
+    for (int cb = 0; cb < 16; ++cb) o[cb] = (f32x16){};
+    m_ref = m_init;
+    l_run = 0.f;
+    l_exact = 0.f;
+    float m_seen = -INFINITY;
+    bool over = false;
+
+    for (int j = 0; j < nsteps; ++j) {
+      const int key0 = key_begin + j * kStepKeys;
+      const int valid = key_end - key0;  // >= 1
+      if (j + 2 < nsteps) wait_vmcnt<2 * L::kLoadsPerStep>();
+      else if (j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
+      else wait_vmcnt<0>();
+      uint8_t LDS_AS* buf = sm + (j & 3) * L::kBuf;
+      if (valid < kStepKeys) {
+        // rows past the history end: P is zero there, V must not be NaN
+        const u32x4 z = {0, 0, 0, 0};
+        const uint32_t row = opaque(dma_row);
+        if ((int)row >= valid) {
+#pragma unroll
+          for (int t = 0; t < L::kLoadsPerStep; ++t)
+            if (!FP8 || 4 * t + wave < L::kSegs) *(u32x4 LDS_AS*)(buf + dma_slot + 4096 * t) = z;
+        }
+      }
+      lds_barrier();
+      if (j + 3 < nsteps)
+        issue_step<FP8>(step_src(j + 3), step_scales(j + 3), src_lane, sm + ((j + 3) & 3) * L::kBuf, wave);
+
+      // ---- S^T = K Q^T (A = K rows from LDS, B = resident query fragment)
+      constexpr int kKPre = 4;
+      bf16x8 kf[kKPre];
+#pragma unroll
+      for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
+      f32x16 s0, s1;
+#pragma unroll
+      for (int ks = 0; ks < 36; ++ks) {
+        const bf16x8 ka = kf[ks % kKPre];
+        if (ks + kKPre < 36) kf[ks % kKPre] = load_k_frag<FP8>(buf, kbase, ks + kKPre);
+        if (ks == 0) mfma_qk<true, FP8>(s0, ka, qf[ks]);
+        else if (ks == 1) mfma_qk<true, FP8>(s1, ka, qf[ks]);
+        else if (ks & 1) mfma_qk<false, FP8>(s1, ka, qf[ks]);
+        else mfma_qk<false, FP8>(s0, ka, qf[ks]);
+      }
+      wait_mfma_vgpr(s0, s1);
+      f32x16 sacc = s0 + s1;
+
+      // ---- online softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3)
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = 8 * (r >> 2) + 4 * h + (r & 3);
+        float x = sacc[r] * c2;
+        if constexpr (FP8) x *= *(const float LDS_AS*)(buf + L::kData + 4 * m);
+        x = m < valid ? x : -INFINITY;
+        sacc[r] = x;
+        mx = fmaxf(mx, x);
+      }
+      mx = fmaxf(mx, wave_xor32(mx));
+      if (m_ref == -INFINITY) m_ref = mx;
+      m_seen = fmaxf(m_seen, mx);
+      over |= mx > m_ref + 64.0f;
+      // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
+      // output by the sum of the rounded weights, so the weights applied to V
+      // sum to one and only the spread of the rounding errors reaches the
+      // output; the LSE keeps the exact fp32 sum.
+      float psum = 0.f, pexact = 0.f;
+      unsigned pb[8];
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        float pa = __builtin_amdgcn_exp2f(sacc[r] - m_ref), pc = __builtin_amdgcn_exp2f(sacc[r + 1] - m_ref);
+        pexact += pa + pc;
+        if constexpr (FP8) {
+          const int ma = 8 * (r >> 2) + 4 * h + (r & 3);
+          const f32x2 sc2 = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * ma);
+          pa = ma < valid ? pa * sc2[0] : 0.f;
+          pc = ma + 1 < valid ? pc * sc2[1] : 0.f;
+          pb[r >> 1] = pack_bf16x2(pa, pc);
+        } else {
+          const unsigned w = pack_bf16x2(pa, pc);
+          pb[r >> 1] = w;
+          psum += __builtin_bit_cast(float, w << 16) + __builtin_bit_cast(float, w & 0xFFFF0000u);
+        }
+      }
+      l_exact += pexact;
+      l_run += FP8 ? pexact : psum;
+      const bf16x8 pB0 = __builtin_bit_cast(bf16x8, (u32x4){pb[0], pb[1], pb[2], pb[3]});
+      const bf16x8 pB1 = __builtin_bit_cast(bf16x8, (u32x4){pb[4], pb[5], pb[6], pb[7]});
+
+      // ---- O^T += V^T P^T.  Key half outer, column block inner, so that
+      // consecutive MFMAs accumulate into different registers; V fragments
+      // are prefetched kVPre MFMAs ahead.
+      constexpr int kVPre = 4;
+      bf16x8 vf[kVPre];
+#pragma unroll
+      for (int x = 0; x < kVPre; ++x) vf[x] = load_v_frag<FP8>(buf, vbase, x & 15, x >> 4);
+#pragma unroll
+      for (int x = 0; x < 32; ++x) {
+        const int cb = x & 15, kh = x >> 4;
+        const bf16x8 va = vf[x % kVPre];
+        if (x + kVPre < 32) vf[x % kVPre] = load_v_frag<FP8>(buf, vbase, (x + kVPre) & 15, (x + kVPre) >> 4);
+        o[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, kh ? pB1 : pB0, o[cb], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
+    __syncthreads();
+    const bool restart = s_restart != 0;
+    __syncthreads();
+    if (!restart) break;
+    if (tid == 0) s_restart = 0;
+    m_init = m_seen;
+    }  // pass
+
+    // ---- epilogue: normalise; final rows as bf16, split units as fp32 partials
+    if (wave_active) {
+      // normaliser: sum of the weights as applied (rounded); LSE: exact sum
+      const float l_tot = l_run + wave_xor32(l_run);
+      const float l_ex = l_exact + wave_xor32(l_exact);
+      const float inv = 1.f / l_tot;
+      const float lse_nat = (m_ref + __log2f(l_ex)) * 0.6931471805599453f;
+      if (head_ok) {
+        if (slot < 0) {
+          uint16_t* orow = (uint16_t*)a.out + ((size_t)tile * a.H + head) * kDimV;
+#pragma unroll
+          for (int cb = 0; cb < 16; ++cb)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+              const int col = 32 * cb + 8 * rg + 4 * h;
+              u32x2 w;
+              w[0] = pack_bf16x2(o[cb][4 * rg] * inv, o[cb][4 * rg + 1] * inv);
+              w[1] = pack_bf16x2(o[cb][4 * rg + 2] * inv, o[cb][4 * rg + 3] * inv);
+              *(u32x2*)(orow + col) = w;
+            }
+          if (h == 0 && a.lse) a.lse[(size_t)tile * a.H + head] = lse_nat;
+        } else {
+          float* prow = a.ws.part_out + ((size_t)slot * a.H + head) * kDimV;
+#pragma unroll
+          for (int cb = 0; cb < 16; ++cb)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+              const int col = 32 * cb + 8 * rg + 4 * h;
+              f32x4 w = {o[cb][4 * rg] * inv, o[cb][4 * rg + 1] * inv, o[cb][4 * rg + 2] * inv,
+                         o[cb][4 * rg + 3] * inv};
+              *(f32x4*)(prow + col) = w;
+            }
+          if (h == 0) a.ws.part_lse[(size_t)slot * a.H + head] = lse_nat;
+        }
+      }
+    }
+  }
+
+  // The last worker to drain the queue re-arms it, so one plan serves many runs.
+  if (tid == 0) {
+    __threadfence();
+    const int32_t done = atomicAdd(&a.ws.header[kHdrDone], 1);
+    if (done == (int32_t)gridDim.x - 1) {
+      atomicExch(&a.ws.header[kHdrGrab], 0);
+      atomicExch(&a.ws.header[kHdrDone], 0);
+    }
+  }
+}
+
+// ============================================================== combine ===
+//
+// One wave per (request or tile, chunk row, head); 8 columns per lane.  The
+// LSE of all parts is reduced across the lanes first; then the partial rows
+// are summed with four parts' loads in flight.
+__global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave_global = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int64_t per_req = (int64_t)c.q_chunk * c.H;
+  const int64_t nreq = c.item_list ? (int64_t)(*c.item_count) : (int64_t)c.B;
+  for (int64_t item = wave_global; item < nreq * per_req; item += nwaves) {
+    const int64_t ri = item / per_req;
+    const int rem = (int)(item - ri * per_req);
+    const int qi = rem / c.H, hh = rem - qi * c.H;
+    const int b = c.item_list ? c.item_list[ri] : (int)ri;
+    const int s0 = c.indptr[b], s1 = c.indptr[b + 1];
+    const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;
+    if (s1 <= s0 && !c.write_empty) continue;
+    const size_t stride = (size_t)c.q_chunk * c.H;           // between parts
+    const size_t base = (size_t)qi * c.H + hh;
+    const float* plse = c.partial_lse + base;
+    float M = -INFINITY;
+    for (int s = s0 + lane; s < s1; s += 64) M = fmaxf(M, plse[(size_t)s * stride]);
+    M = wave_max(M);
+    float wsum = 0.f;
+    if (M > -INFINITY)
+      for (int s = s0 + lane; s < s1; s += 64) wsum += __expf(plse[(size_t)s * stride] - M);
+    wsum = wave_sum(wsum);
+    f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+    if (M > -INFINITY) {
+      const float* prow = c.partials + base * kDimV + 8 * lane;
+      int s = s0;
+      for (; s + 4 <= s1; s += 4) {
+        f32x4 v[8];
+        float w[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const f32x4* src = (const f32x4*)(prow + (size_t)(s + u) * stride * kDimV);
+          v[2 * u] = src[0];
+          v[2 * u + 1] = src[1];
+          w[u] = plse[(size_t)(s + u) * stride];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float wu = __expf(w[u] - M);
+          acc0 += wu * v[2 * u];
+          acc1 += wu * v[2 * u + 1];
+        }
+      }
+      for (; s < s1; ++s) {
+        const f32x4* src = (const f32x4*)(prow + (size_t)s * stride * kDimV);
+        const float wu = __expf(plse[(size_t)s * stride] - M);
+        acc0 += wu * src[0];
+        acc1 += wu * src[1];
+      }
+    }
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    u32x4 w;
+    w[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
+    w[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
+    w[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
+    w[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
+    *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = w;
+    if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+  }
+}
+
+// =============================================================== gather ===
+//
+// Dense copy of every history through the page-address arithmetic of the
+// attend kernel: token j of request b is row (block_table[b][j>>6] << 6) |
+// (j & 63).  One block per request; 16-byte copies.
+__global__ __launch_bounds__(256) void gather_kernel(const uint8_t* kv, const int32_t* bt, const int32_t* seq_lens,
+                                                     int32_t B, int32_t bt_stride, int32_t row_bytes,
+                                                     uint8_t* dense) {
+  const int b = blockIdx.x;
+  size_t off = 0;
+  for (int r = 0; r < b; ++r) off += (size_t)seq_lens[r];
+  const int s = seq_lens[b];
+  const int chunks = row_bytes / 16;
+  for (int64_t e = threadIdx.x; e < (int64_t)s * chunks; e += blockDim.x) {
+    const int j = (int)(e / chunks), ch = (int)(e - (int64_t)j * chunks);
+    const int phys = bt[(size_t)b * bt_stride + (j >> 6)];
+    const uint8_t* src = kv + ((size_t)phys * kPage + (j & 63)) * row_bytes + ch * 16;
+    *(u32x4*)(dense + (off + j) * row_bytes + ch * 16) = *(const u32x4*)src;
+  }
+}
+
+// ================================================================ check ===
+//
+// Validates device data: q_chunk <= seq_lens[b] and every used block-table
+// entry in [0, num_pages).  Writes the smallest failing request + 1 (or 0).
+__global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int32_t* seq_lens, int32_t B,
+                                                    int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
+                                                    int32_t* result) {
+  for (int b = blockIdx.x; b < B; b += gridDim.x) {
+    const int s = seq_lens[b];
+    bool bad = s < q_chunk || (int64_t)(s + kPage - 1) / kPage > bt_stride;
+    if (!bad) {
+      const int np = (s + kPage - 1) / kPage;
+      for (int k = threadIdx.x; k < np; k += blockDim.x) {
+        const int v = bt[(size_t)b * bt_stride + k];
+        if (v < 0 || v >= num_pages) bad = true;
+      }
+    }
+    if (bad) atomicMin(result, b + 1);
+  }
+}
+
+__global__ void init_check(int32_t* result) { *result = INT32_MAX; }
+
+// ============================================================ launchers ===
+
+hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) {
+  if (a.kv_dtype == 1)
+    hipLaunchKernelGGL(attend_kernel<true>, dim3(workers), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(attend_kernel<false>, dim3(workers), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const CombineLaunch& c, hipStream_t s) {
+  int64_t items = (int64_t)c.B * c.q_chunk * c.H;
+  int64_t blocks = (items + 3) / 4;
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)blocks), dim3(256), 0, s, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_lens, int32_t B, int32_t bt_stride,
+                         int32_t row_bytes, void* dense, hipStream_t s) {
+  hipLaunchKernelGGL(gather_kernel, dim3(B), dim3(256), 0, s, (const uint8_t*)kv, bt, seq_lens, B, bt_stride,
+                     row_bytes, (uint8_t*)dense);
+  return hipGetLastError();
+}
+
+hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, int32_t B, int32_t q_chunk, int32_t bt_stride,
+                        int32_t num_pages, int32_t* result, hipStream_t s) {
+  hipLaunchKernelGGL(init_check, dim3(1), dim3(1), 0, s, result);
+  int blocks = B < 1024 ? B : 1024;
+  hipLaunchKernelGGL(check_kernel, dim3(blocks), dim3(256), 0, s, bt, seq_lens, B, q_chunk, bt_stride, num_pages,
+                     result);
+  return hipGetLastError();
+}
+
+}  // namespace splash

@@ -1,0 +1,73 @@
+// Internal launch interface between the C-ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "splash_common.hpp"
+
+namespace splash {
+
+struct Workspace {
+  int32_t* header;      // kHeaderInts ints
+  int4* units;          // [max_units]
+  int32_t* indptr;      // [T + 1]
+  int32_t* split_list;  // [T] tiles that have partials (count in header[2]... see kernels)
+  float* part_lse;      // [max_partials, H]
+  float* part_out;      // [max_partials, H, 512]
+  int32_t max_units;
+  int32_t max_partials;
+};
+
+// Header slots.
+enum HeaderSlot : int {
+  kHdrGrab = 0,        // unit counter the persistent workers draw from
+  kHdrUnits = 1,       // number of work units
+  kHdrPartials = 2,    // partial slots used
+  kHdrChunk = 3,       // pages per unit
+  kHdrDebug = 4,       // device-data check result (0 ok, else first failing item + 1)
+  kHdrDone = 5,        // workers that have drained the queue
+  kHdrSplitTiles = 6,  // number of tiles with partials
+  kHdrTotalPages = 7,
+};
+
+struct PlanLaunch {
+  const int32_t* seq_lens;
+  int32_t B, q_chunk, G, forced_chunk;
+  Workspace ws;
+};
+
+struct AttendLaunch {
+  const void* q;
+  const void* kv;
+  const float* kv_scales;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  void* out;
+  float* lse;
+  int32_t bt_stride, q_chunk, H, kv_dtype, B;
+  float softmax_scale;
+  Workspace ws;
+};
+
+struct CombineLaunch {
+  const float* partials;
+  const float* partial_lse;
+  const int32_t* indptr;     // [B + 1] partial-slot offsets (per request or per tile)
+  const int32_t* item_list;  // optional list of requests to process (count from *item_count)
+  const int32_t* item_count;
+  int32_t B, q_chunk, H;
+  void* out;
+  float* out_lse;
+  bool write_empty;          // requests without partials get out = 0, lse = -inf
+};
+
+hipError_t launch_plan(const PlanLaunch& p, hipStream_t s);
+hipError_t launch_attend(const AttendLaunch& p, int32_t workers, hipStream_t s);
+hipError_t launch_combine(const CombineLaunch& p, hipStream_t s);
+hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_lens, int32_t B,
+                         int32_t bt_stride, int32_t row_bytes, void* dense, hipStream_t s);
+hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, int32_t B, int32_t q_chunk,
+                        int32_t bt_stride, int32_t num_pages, int32_t* result, hipStream_t s);
+
+}  // namespace splash

@@ -1,0 +1,191 @@
+"""The C-ABI library without a GPU: it loads, exports every declared entry
+point, rejects bad arguments with the documented status before touching the
+device, and its host planner produces valid plans."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch  # noqa: F401  (torch's HIP runtime must be loaded before the library)
+
+from paper_2609_37626_amd import binding as B
+from paper_2609_37626_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "splash_attn.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="library not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(splash_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ["splash_mla_attend", "splash_mla_combine", "splash_mla_plan", "splash_mla_run",
+                     "splash_mla_workspace_size", "splash_mla_debug_gather", "splash_status_string"]:
+        assert required in names
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    raw = ctypes.CDLL(B.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(raw, n)]
+    assert not missing, missing
+    assert B.version().startswith("libsplash_attn")
+
+
+FAKE = 1 << 20  # 16-byte aligned non-null address that is never dereferenced
+
+
+def call_attend(desc, q=FAKE, kv=FAKE, bt=FAKE, seq=FAKE, q_chunk=1, out=FAKE, lse=FAKE, ws=FAKE,
+                ws_bytes=1 << 30):
+    L = B.lib()
+    return L.splash_mla_attend(q, kv, bt, seq, q_chunk, out, lse,
+                               None if desc is None else ctypes.byref(desc), ws, ws_bytes, None)
+
+
+def good_desc(**kw):
+    d = B.make_desc(4, 16, 8, 24)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (dict(dim_qk=512), B.SPLASH_ERR_INVALID_ARGUMENT),
+    (dict(dim_v=576), B.SPLASH_ERR_INVALID_ARGUMENT),
+    (dict(page_size=32), B.SPLASH_ERR_UNSUPPORTED),
+    (dict(num_heads=8), B.SPLASH_ERR_UNSUPPORTED),
+    (dict(num_heads=24), B.SPLASH_ERR_UNSUPPORTED),
+    (dict(num_heads=144), B.SPLASH_ERR_UNSUPPORTED),
+    (dict(kv_dtype=7), B.SPLASH_ERR_UNSUPPORTED),
+    (dict(kv_dtype=B.KV_FP8_E4M3), B.SPLASH_ERR_INVALID_ARGUMENT),   # no scales
+    (dict(softmax_scale=float("nan")), B.SPLASH_ERR_INVALID_ARGUMENT),
+    (dict(softmax_scale=0.0), B.SPLASH_ERR_INVALID_ARGUMENT),
+    (dict(max_pages_per_seq=0), B.SPLASH_ERR_INVALID_ARGUMENT),
+    (dict(flags=B.FLAG_FORCE_SPLIT, split_pages=0), B.SPLASH_ERR_INVALID_ARGUMENT),
+    (dict(batch=-1), B.SPLASH_ERR_INVALID_ARGUMENT),
+])
+def test_bad_descriptor_is_rejected(mutate, status):
+    assert call_attend(good_desc(**mutate)) == status
+    assert B.lib().splash_last_error()
+
+
+def test_null_descriptor_and_bad_chunk():
+    assert call_attend(None) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_attend(good_desc(), q_chunk=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+
+
+def test_null_and_misaligned_tensors():
+    assert call_attend(good_desc(), q=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_attend(good_desc(), out=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_attend(good_desc(), q=FAKE + 8) == B.SPLASH_ERR_MISALIGNED
+    assert call_attend(good_desc(), kv=FAKE + 2) == B.SPLASH_ERR_MISALIGNED
+    assert call_attend(good_desc(), ws=FAKE + 4) == B.SPLASH_ERR_MISALIGNED
+
+
+def test_workspace_too_small():
+    need = B.workspace_size(4, 1, 16, 1)
+    assert need > 0
+    base = B.lib().splash_mla_workspace_offsets(4, 1, 16, 0, None)
+    assert base > need
+    assert call_attend(good_desc(), ws_bytes=64) == B.SPLASH_ERR_WORKSPACE_TOO_SMALL
+    # histories longer than one unit's 1024-page cap need room for partials
+    d = good_desc(max_pages_per_seq=2048)
+    small = B.workspace_size(4, 1, 16, 1)
+    assert call_attend(d, ws_bytes=small) == B.SPLASH_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_idle_owner_is_a_noop_even_with_null_pointers():
+    d = good_desc(batch=0)
+    assert call_attend(d, q=0, kv=0, bt=0, seq=0, out=0, lse=0, ws=0, ws_bytes=0) == B.SPLASH_OK
+    L = B.lib()
+    assert L.splash_mla_combine(None, None, None, 0, 1, 16, None, None, None) == B.SPLASH_OK
+
+
+def test_status_strings():
+    L = B.lib()
+    for st in [0, -1, -2, -3, -4, -5]:
+        assert L.splash_status_string(st)
+
+
+def test_workspace_layout_is_aligned_and_ordered():
+    offs, total = B.workspace_offsets(256, 1, 128, 0)
+    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
+    assert total == B.workspace_size(256, 1, 128, 0)
+    assert total >= offs[5] + 1024 * 128 * 512 * 4
+
+
+# ----------------------------------------------------------- host planner ---
+
+def _lengths(cfg):
+    spec = W.CONFIGS[cfg]
+    rng = np.random.Generator(np.random.PCG64(spec.seed))
+    return W.draw_lengths(rng, spec), spec
+
+
+def check_plan(seq_lens, q_chunk, units, indptr, stats, max_partials):
+    T = len(seq_lens) * q_chunk
+    covered = {}
+    slots = []
+    for t, p0, p1, slot in units:
+        assert 0 <= p0 < p1 and p1 - p0 <= 1024
+        covered.setdefault(int(t), []).append((int(p0), int(p1), int(slot)))
+        if slot >= 0:
+            slots.append(int(slot))
+    for t in range(T):
+        b, i = divmod(t, q_chunk)
+        pages = -(-(int(seq_lens[b]) - q_chunk + i + 1) // 64)
+        segs = sorted(covered[t])
+        assert segs[0][0] == 0 and segs[-1][1] == pages
+        assert all(a[1] == c[0] for a, c in zip(segs, segs[1:]))   # contiguous, no overlap
+        if len(segs) == 1:
+            assert segs[0][2] == -1 and indptr[t + 1] == indptr[t]
+        else:
+            assert sorted(s[2] for s in segs) == list(range(indptr[t], indptr[t + 1]))
+    assert len(slots) == len(set(slots)) == stats["partials"] <= max_partials
+    assert stats["units"] == len(units)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_host_plan_covers_every_page_once(cfg):
+    seq, spec = _lengths(cfg)
+    max_pages = int(-(-seq.max() // 64))
+    d = B.make_desc(spec.B, spec.H, max_pages, int((-(-seq // 64)).sum()), spec.kv_dtype,
+                    kv_scales=None)
+    if spec.kv_dtype:
+        d.kv_scales = FAKE
+    units, indptr, stats = B.splash_mla_plan_host(seq, spec.q_chunk, d, 256, 0)
+    check_plan(seq, spec.q_chunk, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+    again = B.splash_mla_plan_host(seq, spec.q_chunk, d, 256, 0)
+    assert np.array_equal(units, again[0]) and np.array_equal(indptr, again[1])
+
+
+def test_host_plan_splits_few_long_and_balances():
+    seq, spec = _lengths(3)
+    d = B.make_desc(4, 128, 1882, 5640)
+    units, _, stats = B.splash_mla_plan_host(seq, 1, d, 256, 0)
+    assert stats["units"] >= 256                    # enough work for every compute unit
+    sizes = units[:, 2] - units[:, 1]
+    assert sizes.max() <= 1.3 * stats["total_pages"] / 256 + 1
+
+
+def test_host_plan_respects_partial_capacity_and_forced_split():
+    seq, spec = _lengths(3)
+    d = B.make_desc(4, 128, 1882, 5640)
+    units, _, stats = B.splash_mla_plan_host(seq, 1, d, 256, 16)
+    assert stats["partials"] <= 16
+    d.flags, d.split_pages = B.FLAG_FORCE_SPLIT, 100
+    units, indptr, stats = B.splash_mla_plan_host(seq, 1, d, 256, 0)
+    assert stats["chunk_pages"] == 100
+    check_plan(seq, 1, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+
+
+def test_host_plan_single_short_request_is_one_unit():
+    d = B.make_desc(1, 16, 1, 1)
+    units, indptr, stats = B.splash_mla_plan_host(np.array([1], np.int32), 1, d, 256, 0)
+    assert units.tolist() == [[0, 0, 1, -1]] and indptr.tolist() == [0, 0]

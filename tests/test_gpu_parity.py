@@ -1,0 +1,273 @@
+"""GPU parity: libsplash_attn through its C-ABI against the fp64 oracle.
+
+Tolerances (the parity bar): outputs max-abs 1e-2 for bf16 caches and 3e-2
+for the fp8 cache, LSE max-abs 1e-3; page resolution and run-to-run results
+bit-exact.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_37626_amd import binding as B
+from paper_2609_37626_amd import workloads as W
+from paper_2609_37626_amd.device import to_device
+
+pytestmark = pytest.mark.gpu
+
+OUT_TOL = {W.KV_BF16: 1e-2, W.KV_FP8_E4M3: 3e-2}
+LSE_TOL = 1e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def run_oracle(batch, **kw):
+    return oracle.mla_attention(batch.q, batch.kv, batch.block_table, batch.seq_lens, batch.q_chunk,
+                                batch.softmax_scale, kv_dtype=batch.kv_dtype, kv_scales=batch.kv_scales, **kw)
+
+
+def gpu_attend(batch, flags=0, split_pages=0, max_partials=0):
+    db = to_device(batch)
+    out, lse = db.alloc_outputs()
+    ws = db.workspace(max_partials)
+    B.splash_mla_attend(db.q, db.kv, db.block_table, db.seq_lens, db.q_chunk, out, lse,
+                        db.desc(flags, split_pages), ws)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def assert_parity(batch, out, lse, ref_out=None, ref_lse=None, label=""):
+    if ref_out is None:
+        ref_out, ref_lse = run_oracle(batch)
+    o = out.float().cpu().numpy()
+    l = lse.cpu().numpy()
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l)), label
+    err_o = np.abs(o - ref_out).max()
+    err_l = np.abs(l - ref_lse).max()
+    print(f"{label}: out max-abs {err_o:.3e}  lse max-abs {err_l:.3e}", flush=True)
+    assert err_o <= OUT_TOL[batch.kv_dtype], (label, err_o)
+    assert err_l <= LSE_TOL, (label, err_l)
+
+
+def lognormal_lengths(seed, n, lo, hi):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return np.clip(np.rint(rng.lognormal(8.0, 1.5, size=n)), lo, hi).astype(np.int32)
+
+
+CASES = {
+    "tiny_cfg1": lambda: W.make_config(1),
+    "many_short_B6_H128": lambda: W.make_custom(
+        np.random.Generator(np.random.PCG64(11)).integers(1024, 4096, size=6, endpoint=True), H=128, seed=11),
+    "ragged_lognormal_B12_with_edges": lambda: W.make_custom(
+        np.concatenate([lognormal_lengths(12, 9, 1, 6000), [1, 64, 65]]), H=128, seed=12),
+    "chunk8_fp8_B3": lambda: W.make_custom([900, 1700, 2500], H=128, q_chunk=8, kv_dtype=W.KV_FP8_E4M3,
+                                           seed=13),
+    "chunk4_bf16_B3": lambda: W.make_custom([4, 129, 1000], H=128, q_chunk=4, seed=14),
+    "heads48_q2": lambda: W.make_custom([70, 300, 2], H=48, q_chunk=2, seed=15),
+    "heads16_single_tokens": lambda: W.make_custom([1, 1, 1], H=16, seed=16),
+    "heads112_fp8_q1": lambda: W.make_custom([33, 640, 1999], H=112, kv_dtype=W.KV_FP8_E4M3, seed=17),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_parity_against_oracle(name):
+    batch = CASES[name]()
+    print(f"case {name}: B={batch.B} H={batch.H} q={batch.q_chunk} lens={batch.seq_lens.tolist()[:12]}", flush=True)
+    out, lse = gpu_attend(batch)
+    assert_parity(batch, out, lse, label=name)
+
+
+@pytest.mark.parametrize("split_pages", [1, 3, 7])
+def test_forced_splits_and_combine(split_pages):
+    batch = W.make_custom([9000, 13001, 65], H=128, seed=21)
+    ref = run_oracle(batch)
+    out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=split_pages)
+    assert_parity(batch, out, lse, *ref, label=f"forced split {split_pages}")
+
+
+def test_forced_splits_fp8_chunk():
+    batch = W.make_custom([700, 2000], H=128, q_chunk=8, kv_dtype=W.KV_FP8_E4M3, seed=22)
+    out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=4)
+    assert_parity(batch, out, lse, label="fp8 chunk forced split")
+
+
+def test_auto_split_single_long_request():
+    batch = W.make_custom([20000], H=128, seed=23)
+    out, lse = gpu_attend(batch)
+    assert_parity(batch, out, lse, label="single long auto split")
+
+
+def test_small_partial_capacity_still_correct():
+    batch = W.make_custom([9000, 13001], H=128, seed=24)
+    out, lse = gpu_attend(batch, max_partials=3)
+    assert_parity(batch, out, lse, label="3 partial slots")
+
+
+def test_poisoned_unused_rows_and_slots_change_nothing():
+    clean = W.make_custom([63, 65, 200, 1], H=128, seed=25, extra_pages=3)
+    poisoned = W.poison_unused_rows(W.make_custom([63, 65, 200, 1], H=128, seed=25, extra_pages=3,
+                                                  unused_slot=W.INT32_MAX))
+    o1, l1 = gpu_attend(clean)
+    o2, l2 = gpu_attend(poisoned)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    assert_parity(clean, o1, l1, label="poison")
+
+
+def test_poisoned_fp8_unused_rows():
+    clean = W.make_custom([63, 100], H=128, q_chunk=2, kv_dtype=W.KV_FP8_E4M3, seed=26, extra_pages=2)
+    poisoned = W.poison_unused_rows(clean)
+    o1, l1 = gpu_attend(clean)
+    o2, l2 = gpu_attend(poisoned)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+
+
+def test_run_to_run_and_page_permutation_bit_identical():
+    batch = W.make_custom([3000, 77, 1500], H=128, seed=27, extra_pages=4)
+    o1, l1 = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=5)
+    o2, l2 = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=5)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    rng = np.random.Generator(np.random.PCG64(99))
+    perm = rng.permutation(batch.num_pages)
+    kv2 = np.empty_like(batch.kv)
+    kv2[perm] = batch.kv
+    bt2 = np.where(batch.block_table >= 0, perm[batch.block_table.clip(0)], -1).astype(np.int32)
+    import dataclasses
+    moved = dataclasses.replace(batch, kv=kv2, block_table=bt2)
+    o3, l3 = gpu_attend(moved, flags=B.FLAG_FORCE_SPLIT, split_pages=5)
+    assert torch.equal(o1.view(torch.int16), o3.view(torch.int16)) and torch.equal(l1, l3)
+
+
+@pytest.mark.parametrize("target", [0, 31, 32, 63, 64, 100, 191])
+def test_dominant_logit_returns_that_latent_bit_exactly(target):
+    """q_rope = k_rope = 8 on one token: its weight rounds to exactly 1 in fp32,
+    so the output is that token's latent, bit for bit, wherever its page sits."""
+    batch = W.make_custom([192], H=16, seed=28)
+    s = 192
+    q = W.f32_to_bf16_bits(np.zeros((1, 16, 576), np.float32))
+    q[..., 512:] = W.f32_to_bf16_bits(np.float32(8.0))
+    kv = batch.kv.copy()
+    phys = lambda j: (int(batch.block_table[0, j // 64]), j % 64)
+    for j in range(s):
+        kv[phys(j)][512:] = 0
+    kv[phys(target)][512:] = W.f32_to_bf16_bits(np.float32(8.0))
+    import dataclasses
+    case = dataclasses.replace(batch, q=q, kv=kv)
+    out, _ = gpu_attend(case)
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got[0, 0], kv[phys(target)][:512])
+    assert np.array_equal(got[0, 15], kv[phys(target)][:512])
+
+
+def test_unit_values_give_unit_output():
+    batch = W.make_custom([300, 5], H=32, seed=29)
+    kv = batch.kv.copy()
+    kv[..., :512] = W.f32_to_bf16_bits(np.float32(1.0))
+    import dataclasses
+    out, _ = gpu_attend(dataclasses.replace(batch, kv=kv))
+    assert np.abs(out.float().cpu().numpy() - 1.0).max() <= 1e-2
+
+
+def test_debug_gather_is_bit_exact():
+    for dtype, batch in [(W.KV_BF16, W.make_custom([1, 64, 65, 300], H=16, seed=30, unused_slot=W.INT32_MAX)),
+                         (W.KV_FP8_E4M3, W.make_custom([129, 7], H=16, kv_dtype=W.KV_FP8_E4M3, seed=31))]:
+        db = to_device(batch)
+        total = int(batch.seq_lens.sum())
+        row_bytes = 1152 if dtype == W.KV_BF16 else 576
+        dense = torch.zeros((total, row_bytes), dtype=torch.uint8, device="cuda")
+        B.splash_mla_debug_gather(db.kv, db.block_table, db.seq_lens, db.desc(), dense)
+        torch.cuda.synchronize()
+        flat = batch.kv.reshape(batch.num_pages * 64, -1)
+        rows = []
+        for b, s in enumerate(batch.seq_lens):
+            j = np.arange(int(s))
+            rows.append(flat[batch.block_table[b, j // 64].astype(np.int64) * 64 + j % 64])
+        want = np.concatenate(rows).view(np.uint8).reshape(total, row_bytes)
+        assert np.array_equal(dense.cpu().numpy(), want)
+
+
+def test_device_plan_matches_host_plan():
+    spec = W.CONFIGS[4]
+    rng = np.random.Generator(np.random.PCG64(spec.seed))
+    seq = W.draw_lengths(rng, spec)
+    d = B.make_desc(spec.B, spec.H, int(-(-seq.max() // 64)), int((-(-seq // 64)).sum()))
+    ws = torch.zeros(B.workspace_size(spec.B, 1, spec.H, 0), dtype=torch.uint8, device="cuda")
+    B.splash_mla_plan(torch.from_numpy(seq).cuda(), 1, d, ws)
+    torch.cuda.synchronize()
+    units, indptr, stats = B.splash_mla_plan_host(seq, 1, d, B.device_workers(), 0)
+    offs, _ = B.workspace_offsets(spec.B, 1, spec.H, 0)
+    raw = ws.cpu().numpy()
+    hdr = raw[offs[0]:offs[0] + 256].view(np.int32)
+    assert hdr[1] == stats["units"] and hdr[2] == stats["partials"] and hdr[3] == stats["chunk_pages"]
+    dev_units = raw[offs[1]:offs[1] + 16 * stats["units"]].view(np.int32).reshape(-1, 4)
+    assert np.array_equal(dev_units, units)
+    dev_indptr = raw[offs[2]:offs[2] + 4 * (spec.B + 1)].view(np.int32)
+    assert np.array_equal(dev_indptr, indptr)
+
+
+def test_plan_once_run_many():
+    batch = W.make_custom([5000, 300, 64], H=128, seed=32)
+    db = to_device(batch)
+    ws = db.workspace()
+    d = db.desc()
+    B.splash_mla_plan(db.seq_lens, 1, d, ws)
+    outs = []
+    for _ in range(3):
+        out, lse = db.alloc_outputs()
+        B.splash_mla_run(db.q, db.kv, db.block_table, db.seq_lens, 1, out, lse, d, ws)
+        outs.append((out, lse))
+    torch.cuda.synchronize()
+    for out, lse in outs[1:]:
+        assert torch.equal(out.view(torch.int16), outs[0][0].view(torch.int16)) and torch.equal(lse, outs[0][1])
+    assert_parity(batch, *outs[0], label="plan once, run three times")
+
+
+def test_standalone_combine_matches_oracle_merge():
+    batch = W.make_custom([500, 240], H=16, q_chunk=2, seed=33)
+    cuts = {0: [0, 100, 101, 500], 1: [0, 240, 240]}        # includes an empty part
+    parts_o, parts_l, indptr = [], [], [0]
+    for b in range(batch.B):
+        for lo, hi in zip(cuts[b][:-1], cuts[b][1:]):
+            kr = np.zeros((batch.B, 2), np.int64)
+            kr[b] = (lo, hi)
+            o, l = run_oracle(batch, requests=[b], key_ranges=kr)
+            parts_o.append(np.nan_to_num(o[b * 2:(b + 1) * 2]))
+            parts_l.append(l[b * 2:(b + 1) * 2])
+        indptr.append(indptr[-1] + len(cuts[b]) - 1)
+    partials = torch.tensor(np.stack(parts_o), dtype=torch.float32, device="cuda")
+    plse = torch.tensor(np.stack(parts_l), dtype=torch.float32, device="cuda")
+    ip = torch.tensor(indptr, dtype=torch.int32, device="cuda")
+    out = torch.empty((batch.B * 2, 16, 512), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((batch.B * 2, 16), dtype=torch.float32, device="cuda")
+    B.splash_mla_combine(partials, plse, ip, batch.B, 2, 16, out, lse)
+    torch.cuda.synchronize()
+    assert_parity(batch, out, lse, label="standalone combine")
+
+
+def test_idle_owner_on_gpu():
+    d = B.make_desc(0, 128, 1, 1)
+    ws = torch.zeros(1024, dtype=torch.uint8, device="cuda")
+    B.splash_mla_attend(None, None, None, None, 1, None, None, d, ws)
+
+
+def test_debug_check_rejects_bad_device_data():
+    batch = W.make_custom([100, 300], H=16, seed=34)
+    bad = batch.block_table.copy()
+    bad[1, 2] = batch.num_pages + 5                          # outside the pool
+    import dataclasses
+    db = to_device(dataclasses.replace(batch, block_table=bad))
+    out, lse = db.alloc_outputs()
+    with pytest.raises(B.SplashError) as e:
+        B.splash_mla_attend(db.q, db.kv, db.block_table, db.seq_lens, 1, out, lse,
+                            db.desc(flags=B.FLAG_DEBUG_CHECK), db.workspace())
+    assert e.value.status == B.SPLASH_ERR_INVALID_ARGUMENT
+    good = to_device(batch)
+    out, lse = good.attend(flags=B.FLAG_DEBUG_CHECK)
+    torch.cuda.synchronize()
+    assert_parity(batch, out, lse, label="debug check passes good data")
