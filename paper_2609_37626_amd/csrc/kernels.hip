@@ -258,23 +258,35 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
 
 // =============================================================== attend ===
 //
-// LDS layout of one staged step (32 cache rows): chunk-major.  A row is 72
-// (bf16) or 36 (fp8) 16-byte chunks; chunk c of row r sits at byte
-//   c * 512 + (r ^ swz(c)) * 16,   swz(c) = 4*(c & 1) ^ 8*((c >> 1) & 1).
-// Each 1 KB direct-to-LDS load instruction then fills chunks 2s, 2s+1 of all
-// 32 rows, every operand read below is a lane-dependent base plus an
-// immediate, and the row XOR keeps the transposing reads conflict-free.
+// Work split inside a workgroup (4 waves, one per SIMD):
+//  * S^T = K Q^T: wave w owns heads [32w, 32w+32) (its query fragment stays in
+//    VGPRs) and computes their scores and softmax;
+//  * P goes through LDS; O^T += V^T P^T: wave w owns output columns
+//    [128w, 128w+128) for all 128 heads, so each wave transposes only a
+//    quarter of V out of LDS.
+//
+// LDS layout of one staged step (32 cache rows): rows are cut into line
+// groups of 128 B (bf16) or 64 B (fp8); group g of row r sits at
+//   bf16: g*4096 + r*128 + ((c8 ^ ((r >> 1) & 7)) * 16)     (c8 = chunk in group)
+//   fp8:  g*2048 + r*64  + ((c4 ^ ((r >> 1) & 3)) * 16)
+// so every 1 KB direct-to-LDS instruction reads whole memory lines of 8 (16)
+// rows, and the XOR spreads the operand reads over the LDS banks.
 
 template <bool FP8>
 struct StepLayout {
   static constexpr int kRowBytes = FP8 ? kDimQK : 2 * kDimQK;       // 576 / 1152
-  static constexpr int kChunks = kRowBytes / 16;                     // 36 / 72
+  static constexpr int kGroupBytes = FP8 ? 64 : 128;                 // memory line group
+  static constexpr int kGroupStride = kStepKeys * kGroupBytes;       // 2048 / 4096
   static constexpr int kData = kStepKeys * kRowBytes;                // 18432 / 36864
   static constexpr int kBuf = FP8 ? kData + 256 : kData;             // + fp32 scales
   static constexpr int kBufs = 4;
-  static constexpr int kSegs = kChunks / 2;                          // 1 KB segments: 18 / 36
   static constexpr int kLoadsPerStep = FP8 ? 5 : 9;                  // per wave
+  static constexpr int kRing = kBufs * kBuf;
 };
+
+// LDS map beyond the ring (bytes)
+constexpr int kPBytes = kMaxHeads * kStepKeys * 2;   // P for all heads, bf16
+constexpr int kRingMax = 4 * 36864;
 
 // Direct global->LDS loads, issued through asm so that the compiler's wait
 // insertion (which cannot tell which LDS bytes they write) does not drain
@@ -300,26 +312,27 @@ __device__ __forceinline__ void dma_b32(const void* gptr, const uint8_t LDS_AS* 
       : "memory");
 }
 
-__device__ __forceinline__ uint32_t chunk_swz(uint32_t c) { return 4u * (c & 1u) ^ 8u * ((c >> 1) & 1u); }
-
-// Issue the direct-to-LDS loads of one step.  Wave w fills segments
-// s = 4t + w; lane l writes row slot (l & 31) of chunk 2s + (l >> 5), which
-// holds logical row (l & 31) ^ swz(chunk).  src_lane is the lane's byte
-// offset inside the step for t = 0 (see attend_kernel).
+// Issue the direct-to-LDS loads of one step.
+//  bf16: wave w loads rows [8w, 8w+8) of every line group g (t = g);
+//  fp8:  instruction i = w + 4t (< 18) loads line group i >> 1, rows
+//        [16 (i & 1), +16); waves 2 and 3 also load the 32 token scales.
+// src_lane is the lane's byte offset inside the step for t = 0.
 template <bool FP8>
 __device__ __forceinline__ void issue_step(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                            uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
-  using L = StepLayout<FP8>;
+  if constexpr (!FP8) {
 #pragma unroll
-  for (int t = 0; t < L::kLoadsPerStep; ++t) {
-    const int seg = 4 * t + wave;
-    if (!FP8 || t < 4 || seg < L::kSegs) {
-      dma_b128(step_src + src_lane + 128 * t, buf + 4096 * t + 1024 * wave);
-    } else {
-      // waves 2 and 3: the step's 32 per-token scales (lanes 32..63 repeat
-      // them; both waves write identical bytes to the same place).
-      const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
-      dma_b32(step_scales + (lane & 31), buf + L::kData);
+    for (int t = 0; t < 9; ++t) dma_b128(step_src + src_lane + 128 * t, buf + 4096 * t + 1024 * wave);
+  } else {
+#pragma unroll
+    for (int t = 0; t < 5; ++t) {
+      const int i = wave + 4 * t;
+      if (t < 4 || i < 18) {
+        dma_b128(step_src + src_lane + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+      } else {
+        const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+        dma_b32(step_scales + (lane & 31), buf + 18432);
+      }
     }
   }
 }
@@ -352,10 +365,8 @@ __device__ __forceinline__ void wait_mfma_vgpr(f32x16& a0, f32x16& a1) {
 template <bool FP8>
 __device__ __forceinline__ bf16x8 load_k_frag(const uint8_t LDS_AS* buf, const uint32_t* kbase, int ks) {
   if constexpr (!FP8) {
-    // chunk 2ks + h; base chosen by ks parity
-    return *(const bf16x8 LDS_AS*)(buf + kbase[ks & 1] + 1024 * ks);
+    return *(const bf16x8 LDS_AS*)(buf + kbase[ks & 3] + 4096 * (ks >> 2));
   } else {
-    // chunk ks, half h; base chosen by ks & 3
     const u32x2 raw = *(const u32x2 LDS_AS*)(buf + kbase[ks & 3] + 2048 * (ks >> 2));
     return fp8x8_to_bf16(raw);
   }
@@ -363,80 +374,98 @@ __device__ __forceinline__ bf16x8 load_k_frag(const uint8_t LDS_AS* buf, const u
 
 // V^T operand fragment (column block cb, key half kh) via transposing reads.
 template <bool FP8>
-__device__ __forceinline__ bf16x8 load_v_frag(const uint8_t LDS_AS* buf, const uint32_t* vbase, int cb, int kh) {
+__device__ __forceinline__ bf16x8 load_v_frag(const uint8_t LDS_AS* buf, const uint32_t (*vbase)[2], int cb, int kh) {
   if constexpr (!FP8) {
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 LDS_AS*)(buf + vbase[0] + 2048 * cb + 256 * kh));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 LDS_AS*)(buf + vbase[1] + 2048 * cb + 256 * kh));
+    const uint8_t LDS_AS* p = buf + 4096 * (cb >> 1) + 2048 * kh;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 LDS_AS*)(p + vbase[cb & 1][0]));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4 LDS_AS*)(p + vbase[cb & 1][1]));
     const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
     return __builtin_bit_cast(bf16x8, (u32x4){l2[0], l2[1], h2[0], h2[1]});
   } else {
-    const i32x2 raw =
-        __builtin_amdgcn_ds_read_tr8_b64_v2i32((i32x2 LDS_AS*)(buf + vbase[cb & 1] + 2048 * (cb >> 1) + 256 * kh));
+    const i32x2 raw = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+        (i32x2 LDS_AS*)(buf + vbase[cb & 1][0] + 2048 * (cb >> 1) + 1024 * kh));
     return fp8x8_to_bf16(__builtin_bit_cast(u32x2, raw));
   }
+}
+
+// P^T operand fragment (head block hb, key half kh) from the P exchange area:
+// head hh's 32 weights are 64 B, slot (kh, half) at ((2kh + half) ^ (hh>>2 & 3)) * 16.
+__device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t half) {
+  return hh * 64 + (((2 * kh + half) ^ ((hh >> 2) & 3)) * 16);
 }
 
 template <bool FP8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   using L = StepLayout<FP8>;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[L::kBufs * L::kBuf];
-  __shared__ int32_t s_bt[kMaxUnitPages];
+  constexpr int kStage = 128 * 1040 > 64 * 2064 ? 128 * 1040 : 64 * 2064;  // epilogue staging
+  constexpr int kPOff = L::kRing > kStage ? L::kRing : kStage;
+  constexpr int kLOff = kPOff + kPBytes;            // per-head normaliser, 128 floats
+  constexpr int kBtOff = kLOff + kMaxHeads * 4;     // block-table slice
+  constexpr int kSmem = kBtOff + kMaxUnitPages * 4;
+  static_assert(kSmem <= 163840 - 64, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
   __shared__ int4 s_unit;
   __shared__ int32_t s_restart;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int h = lane >> 5, n32 = lane & 31;
-  const int head = wave * 32 + n32;
+  const int head = wave * 32 + n32;                           // head of the QK/softmax role
   const bool head_ok = head < a.H;
-  const bool wave_active = wave * 32 < a.H;
   const int32_t num_units = a.ws.header[kHdrUnits];
   if (tid == 0) s_restart = 0;
   const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
+  uint8_t LDS_AS* p_lds = sm + kPOff;
+  float LDS_AS* l_lds = (float LDS_AS*)(sm + kLOff);
+  int32_t LDS_AS* s_bt = (int32_t LDS_AS*)(sm + kBtOff);
 
-  // ---- per-lane LDS / global offsets (bytes), fixed for the kernel ----
-  // DMA: segment s = 4t + wave holds chunk c = 2s + h, row slot n32, i.e.
-  // logical row n32 ^ swz(c) with swz(c) = 4h ^ 8*(wave & 1).
-  const uint32_t dma_row = n32 ^ (4u * h) ^ (8u * (wave & 1));
-  const uint32_t src_lane = dma_row * L::kRowBytes + (2 * wave + h) * 16;
-  // Row this lane's DMA slots hold (for zeroing rows past the history end).
-  const uint32_t dma_slot = 1024 * wave + 16 * lane;
-  // K operand.
-  uint32_t kbase[4];
+  // ---- per-lane offsets (bytes), fixed for the kernel ----
+  uint32_t src_lane, dma_row, dma_slot;
   if constexpr (!FP8) {
-#pragma unroll
-    for (int par = 0; par < 2; ++par) {
-      const uint32_t c = 2 * par + h;                 // chunk 2ks + h, ks even/odd
-      kbase[par] = h * 512 + (n32 ^ chunk_swz(c)) * 16 + 0 * c;
-    }
-    kbase[2] = kbase[3] = 0;
+    dma_row = 8 * wave + (lane >> 3);
+    src_lane = dma_row * 1152 + (((lane & 7) ^ ((dma_row >> 1) & 7)) * 16);
+    dma_slot = 1024 * wave + 16 * lane;              // + 4096 t
   } else {
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) kbase[r4] = r4 * 512 + (n32 ^ chunk_swz(r4)) * 16 + 8 * h;
+    dma_row = 16 * (wave & 1) + (lane >> 2);
+    src_lane = dma_row * 576 + 64 * (wave >> 1) + (((lane & 3) ^ ((dma_row >> 1) & 3)) * 16);
+    dma_slot = 2048 * (wave >> 1) + 1024 * (wave & 1) + 16 * lane;   // + 4096 t
   }
-  // V operand.
-  const int i16 = lane & 15, g = lane >> 4;
-  uint32_t vbase[2];
+  // K operand: row n32, chunk 2ks + h (bf16) / 16-byte chunk ks, half h (fp8)
+  uint32_t kbase[4];
+#pragma unroll
+  for (int r4 = 0; r4 < 4; ++r4) {
+    if constexpr (!FP8)
+      kbase[r4] = n32 * 128 + (((2 * r4 + h) ^ ((n32 >> 1) & 7)) * 16);
+    else
+      kbase[r4] = n32 * 64 + ((r4 ^ ((n32 >> 1) & 3)) * 16) + 8 * h;
+  }
+  // V operand (transposing reads), see load_v_frag
+  const int i16 = lane & 15, g16 = lane >> 4;
+  uint32_t vbase[2][2];
   if constexpr (!FP8) {
-    // tr16: source lane supplies row 16kh + 8t + 4h + (i16>>2), columns
-    // 32cb + 16(g&1) + 4(i16&3) .. +4, i.e. chunk 4cb + cc, 8*(i16&1) bytes in.
-    const uint32_t cc = 2 * (g & 1) + ((i16 >> 1) & 1);
-    const uint32_t sw = chunk_swz(cc);                  // swz(4cb + cc) = swz(cc)
+    // source lane: row 16kh + 8t + 4h + (i16>>2), chunk 4cb + cc, 8*(i16&1) bytes in
+    const uint32_t cc = 2 * (g16 & 1) + ((i16 >> 1) & 1);
     const uint32_t rb = 4 * h + (i16 >> 2);
 #pragma unroll
-    for (int t = 0; t < 2; ++t) vbase[t] = cc * 512 + ((8 * t + rb) ^ sw) * 16 + 8 * (i16 & 1);
+    for (int cbo = 0; cbo < 2; ++cbo)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const uint32_t row = 8 * t + rb;
+        vbase[cbo][t] = row * 128 + (((4 * cbo + cc) ^ ((row >> 1) & 7)) * 16) + 8 * (i16 & 1);
+      }
   } else {
-    // tr8: source lane s supplies key k = s>>1 of the slot order (rows
-    // 8(k>>2) + 4h + (k&3)), 8 bytes of chunk 2cb + (g&1).
+    // tr8 source lane: key k = i16>>1 of the slot order, 8 columns at
+    // 32cb + 16(g16&1) + 8(i16&1), i.e. 16-byte chunk 2cb + (g16&1)
     const int k = i16 >> 1;
     const uint32_t rowk = 8 * (k >> 2) + 4 * h + (k & 3);
 #pragma unroll
-    for (int cbp = 0; cbp < 2; ++cbp) {
-      const uint32_t c = 2 * cbp + (g & 1);
-      vbase[cbp] = c * 512 + (rowk ^ chunk_swz(c)) * 16 + 8 * (i16 & 1);
+    for (int cbo = 0; cbo < 2; ++cbo) {
+      const uint32_t c4 = 2 * cbo + (g16 & 1);
+      vbase[cbo][0] = rowk * 64 + ((c4 ^ ((rowk >> 1) & 3)) * 16) + 8 * (i16 & 1);
+      vbase[cbo][1] = 0;
     }
   }
 
@@ -486,167 +515,209 @@ void attend_kernel(AttendLaunch a) {
       const int phys = s_bt[(key >> 6) - p0];
       return a.kv_scales + (size_t)phys * kPage + ((key >> 5) & 1) * kStepKeys;
     };
+
     // Softmax reference: fixed at the first step's max (O is still zero
     // there), never moved afterwards, so O is never rescaled inside the loop.
     // If a later logit exceeds it by more than 64 (base 2), P could overflow:
     // the workgroup then redoes the unit with the unit's true max, which is
     // known after the first pass.
     float m_init = -INFINITY;
-    f32x16 o[16];
+    f32x16 o[4][4];  // [column block cb - 4*wave][head block]
     float m_ref, l_run, l_exact;
     for (;;) {
 #pragma unroll
-    for (int j = 0; j < 3; ++j)
-      if (j < nsteps) issue_step<FP8>(step_src(j), step_scales(j), src_lane, sm + j * L::kBuf, wave);
+      for (int j = 0; j < 3; ++j)
+        if (j < nsteps) issue_step<FP8>(step_src(j), step_scales(j), src_lane, sm + j * L::kBuf, wave);
 
 #pragma unroll
-    for (int cb = 0; cb < 16; ++cb) o[cb] = (f32x16){};
-    m_ref = m_init;
-    l_run = 0.f;
-    l_exact = 0.f;
-    float m_seen = -INFINITY;
-    bool over = false;
-
-    for (int j = 0; j < nsteps; ++j) {
-      const int key0 = key_begin + j * kStepKeys;
-      const int valid = key_end - key0;  // >= 1
-      if (j + 2 < nsteps) wait_vmcnt<2 * L::kLoadsPerStep>();
-      else if (j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
-      else wait_vmcnt<0>();
-      uint8_t LDS_AS* buf = sm + (j & 3) * L::kBuf;
-      if (valid < kStepKeys) {
-        // rows past the history end: P is zero there, V must not be NaN
-        const u32x4 z = {0, 0, 0, 0};
-        const uint32_t row = opaque(dma_row);
-        if ((int)row >= valid) {
+      for (int x = 0; x < 4; ++x)
 #pragma unroll
-          for (int t = 0; t < L::kLoadsPerStep; ++t)
-            if (!FP8 || 4 * t + wave < L::kSegs) *(u32x4 LDS_AS*)(buf + dma_slot + 4096 * t) = z;
+        for (int y = 0; y < 4; ++y) o[x][y] = (f32x16){};
+      m_ref = m_init;
+      l_run = 0.f;
+      l_exact = 0.f;
+      float m_seen = -INFINITY;
+      bool over = false;
+
+      for (int j = 0; j < nsteps; ++j) {
+        const int key0 = key_begin + j * kStepKeys;
+        const int valid = key_end - key0;  // >= 1
+        if (j + 2 < nsteps) wait_vmcnt<2 * L::kLoadsPerStep>();
+        else if (j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
+        else wait_vmcnt<0>();
+        uint8_t LDS_AS* buf = sm + (j & 3) * L::kBuf;
+        if (valid < kStepKeys) {
+          // rows past the history end: P is zero there, V must not be NaN
+          const u32x4 z = {0, 0, 0, 0};
+          if ((int)opaque(dma_row) >= valid) {
+#pragma unroll
+            for (int t = 0; t < L::kLoadsPerStep; ++t)
+              if (!FP8 || t < 4 || wave + 4 * t < 18) *(u32x4 LDS_AS*)(buf + dma_slot + 4096 * t) = z;
+          }
+        }
+        lds_barrier();  // step j staged; every wave is past step j-1
+        if (j + 3 < nsteps)
+          issue_step<FP8>(step_src(j + 3), step_scales(j + 3), src_lane, sm + ((j + 3) & 3) * L::kBuf, wave);
+
+        // ---- S^T = K Q^T (A = K rows from LDS, B = resident query fragment)
+        constexpr int kKPre = 4;
+        bf16x8 kf[kKPre];
+#pragma unroll
+        for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
+        f32x16 s0, s1;
+#pragma unroll
+        for (int ks = 0; ks < 36; ++ks) {
+          const bf16x8 ka = kf[ks % kKPre];
+          if (ks + kKPre < 36) kf[ks % kKPre] = load_k_frag<FP8>(buf, kbase, ks + kKPre);
+          if (ks == 0) mfma_qk<true, FP8>(s0, ka, qf[ks]);
+          else if (ks == 1) mfma_qk<true, FP8>(s1, ka, qf[ks]);
+          else if (ks & 1) mfma_qk<false, FP8>(s1, ka, qf[ks]);
+          else mfma_qk<false, FP8>(s0, ka, qf[ks]);
+        }
+        wait_mfma_vgpr(s0, s1);
+        f32x16 sacc = s0 + s1;
+
+        // ---- online softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3)
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = 8 * (r >> 2) + 4 * h + (r & 3);
+          float x = sacc[r] * c2;
+          if constexpr (FP8) x *= *(const float LDS_AS*)(buf + L::kData + 4 * m);
+          x = m < valid ? x : -INFINITY;
+          sacc[r] = x;
+          mx = fmaxf(mx, x);
+        }
+        mx = fmaxf(mx, wave_xor32(mx));
+        if (m_ref == -INFINITY) m_ref = mx;
+        m_seen = fmaxf(m_seen, mx);
+        over |= mx > m_ref + 64.0f;
+        // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
+        // output by the sum of the rounded weights, so the weights applied to V
+        // sum to one and only the spread of the rounding errors reaches the
+        // output; the LSE keeps the exact fp32 sum.
+        float psum = 0.f, pexact = 0.f;
+        unsigned pb[8];
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          float pa = __builtin_amdgcn_exp2f(sacc[r] - m_ref), pc = __builtin_amdgcn_exp2f(sacc[r + 1] - m_ref);
+          pexact += pa + pc;
+          if constexpr (FP8) {
+            const int ma = 8 * (r >> 2) + 4 * h + (r & 3);
+            const f32x2 sc2 = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * ma);
+            pa = ma < valid ? pa * sc2[0] : 0.f;
+            pc = ma + 1 < valid ? pc * sc2[1] : 0.f;
+            pb[r >> 1] = pack_bf16x2(pa, pc);
+          } else {
+            const unsigned w = pack_bf16x2(pa, pc);
+            pb[r >> 1] = w;
+            psum += __builtin_bit_cast(float, w << 16) + __builtin_bit_cast(float, w & 0xFFFF0000u);
+          }
+        }
+        l_exact += pexact;
+        l_run += FP8 ? pexact : psum;
+        // publish this wave's P^T (keys in slot order) for every wave's PV
+        *(u32x4 LDS_AS*)(p_lds + p_slot(head, 0, h)) = (u32x4){pb[0], pb[1], pb[2], pb[3]};
+        *(u32x4 LDS_AS*)(p_lds + p_slot(head, 1, h)) = (u32x4){pb[4], pb[5], pb[6], pb[7]};
+        lds_barrier();  // P of all heads visible
+
+        // ---- O^T[cols of this wave, all heads] += V^T P^T
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh) {
+          bf16x8 pf[4];
+#pragma unroll
+          for (int hb = 0; hb < 4; ++hb)
+            pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, kh, h));
+          bf16x8 vf = load_v_frag<FP8>(buf, vbase, 4 * wave, kh);
+#pragma unroll
+          for (int cbl = 0; cbl < 4; ++cbl) {
+            const bf16x8 va = vf;
+            if (cbl < 3) vf = load_v_frag<FP8>(buf, vbase, 4 * wave + cbl + 1, kh);
+#pragma unroll
+            for (int hb = 0; hb < 4; ++hb)
+              o[cbl][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[hb], o[cbl][hb], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
       }
-      lds_barrier();
-      if (j + 3 < nsteps)
-        issue_step<FP8>(step_src(j + 3), step_scales(j + 3), src_lane, sm + ((j + 3) & 3) * L::kBuf, wave);
-
-      // ---- S^T = K Q^T (A = K rows from LDS, B = resident query fragment)
-      constexpr int kKPre = 4;
-      bf16x8 kf[kKPre];
-#pragma unroll
-      for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
-      f32x16 s0, s1;
-#pragma unroll
-      for (int ks = 0; ks < 36; ++ks) {
-        const bf16x8 ka = kf[ks % kKPre];
-        if (ks + kKPre < 36) kf[ks % kKPre] = load_k_frag<FP8>(buf, kbase, ks + kKPre);
-        if (ks == 0) mfma_qk<true, FP8>(s0, ka, qf[ks]);
-        else if (ks == 1) mfma_qk<true, FP8>(s1, ka, qf[ks]);
-        else if (ks & 1) mfma_qk<false, FP8>(s1, ka, qf[ks]);
-        else mfma_qk<false, FP8>(s0, ka, qf[ks]);
-      }
-      wait_mfma_vgpr(s0, s1);
-      f32x16 sacc = s0 + s1;
-
-      // ---- online softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3)
-      float mx = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = 8 * (r >> 2) + 4 * h + (r & 3);
-        float x = sacc[r] * c2;
-        if constexpr (FP8) x *= *(const float LDS_AS*)(buf + L::kData + 4 * m);
-        x = m < valid ? x : -INFINITY;
-        sacc[r] = x;
-        mx = fmaxf(mx, x);
-      }
-      mx = fmaxf(mx, wave_xor32(mx));
-      if (m_ref == -INFINITY) m_ref = mx;
-      m_seen = fmaxf(m_seen, mx);
-      over |= mx > m_ref + 64.0f;
-      // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
-      // output by the sum of the rounded weights, so the weights applied to V
-      // sum to one and only the spread of the rounding errors reaches the
-      // output; the LSE keeps the exact fp32 sum.
-      float psum = 0.f, pexact = 0.f;
-      unsigned pb[8];
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        float pa = __builtin_amdgcn_exp2f(sacc[r] - m_ref), pc = __builtin_amdgcn_exp2f(sacc[r + 1] - m_ref);
-        pexact += pa + pc;
-        if constexpr (FP8) {
-          const int ma = 8 * (r >> 2) + 4 * h + (r & 3);
-          const f32x2 sc2 = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * ma);
-          pa = ma < valid ? pa * sc2[0] : 0.f;
-          pc = ma + 1 < valid ? pc * sc2[1] : 0.f;
-          pb[r >> 1] = pack_bf16x2(pa, pc);
-        } else {
-          const unsigned w = pack_bf16x2(pa, pc);
-          pb[r >> 1] = w;
-          psum += __builtin_bit_cast(float, w << 16) + __builtin_bit_cast(float, w & 0xFFFF0000u);
-        }
-      }
-      l_exact += pexact;
-      l_run += FP8 ? pexact : psum;
-      const bf16x8 pB0 = __builtin_bit_cast(bf16x8, (u32x4){pb[0], pb[1], pb[2], pb[3]});
-      const bf16x8 pB1 = __builtin_bit_cast(bf16x8, (u32x4){pb[4], pb[5], pb[6], pb[7]});
-
-      // ---- O^T += V^T P^T.  Key half outer, column block inner, so that
-      // consecutive MFMAs accumulate into different registers; V fragments
-      // are prefetched kVPre MFMAs ahead.
-      constexpr int kVPre = 4;
-      bf16x8 vf[kVPre];
-#pragma unroll
-      for (int x = 0; x < kVPre; ++x) vf[x] = load_v_frag<FP8>(buf, vbase, x & 15, x >> 4);
-#pragma unroll
-      for (int x = 0; x < 32; ++x) {
-        const int cb = x & 15, kh = x >> 4;
-        const bf16x8 va = vf[x % kVPre];
-        if (x + kVPre < 32) vf[x % kVPre] = load_v_frag<FP8>(buf, vbase, (x + kVPre) & 15, (x + kVPre) >> 4);
-        o[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, kh ? pB1 : pB0, o[cb], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
-    __syncthreads();
-    const bool restart = s_restart != 0;
-    __syncthreads();
-    if (!restart) break;
-    if (tid == 0) s_restart = 0;
-    m_init = m_seen;
+      if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
+      __syncthreads();
+      const bool restart = s_restart != 0;
+      __syncthreads();
+      if (!restart) break;
+      if (tid == 0) s_restart = 0;
+      m_init = m_seen;
     }  // pass
 
-    // ---- epilogue: normalise; final rows as bf16, split units as fp32 partials
-    if (wave_active) {
+    // ---- epilogue: normalise, stage through LDS, write whole rows
+    {
       // normaliser: sum of the weights as applied (rounded); LSE: exact sum
       const float l_tot = l_run + wave_xor32(l_run);
       const float l_ex = l_exact + wave_xor32(l_exact);
-      const float inv = 1.f / l_tot;
       const float lse_nat = (m_ref + __log2f(l_ex)) * 0.6931471805599453f;
-      if (head_ok) {
+      if (h == 0) l_lds[head] = l_tot;
+      if (h == 0 && head_ok) {
         if (slot < 0) {
-          uint16_t* orow = (uint16_t*)a.out + ((size_t)tile * a.H + head) * kDimV;
-#pragma unroll
-          for (int cb = 0; cb < 16; ++cb)
-#pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-              const int col = 32 * cb + 8 * rg + 4 * h;
-              u32x2 w;
-              w[0] = pack_bf16x2(o[cb][4 * rg] * inv, o[cb][4 * rg + 1] * inv);
-              w[1] = pack_bf16x2(o[cb][4 * rg + 2] * inv, o[cb][4 * rg + 3] * inv);
-              *(u32x2*)(orow + col) = w;
-            }
-          if (h == 0 && a.lse) a.lse[(size_t)tile * a.H + head] = lse_nat;
+          if (a.lse) a.lse[(size_t)tile * a.H + head] = lse_nat;
         } else {
-          float* prow = a.ws.part_out + ((size_t)slot * a.H + head) * kDimV;
+          a.ws.part_lse[(size_t)slot * a.H + head] = lse_nat;
+        }
+      }
+    }
+    __syncthreads();
+    float inv[4];
 #pragma unroll
-          for (int cb = 0; cb < 16; ++cb)
+    for (int hb = 0; hb < 4; ++hb) inv[hb] = 1.f / l_lds[32 * hb + n32];
+    const int nrows = a.H;  // rows (heads) of this tile that exist
+    if (slot < 0) {
+      // bf16 [head][512] rows, stride 1040 B in LDS
+      constexpr int kStride = 1040;
+#pragma unroll
+      for (int cbl = 0; cbl < 4; ++cbl)
+#pragma unroll
+        for (int hb = 0; hb < 4; ++hb)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
+            const int hh = 32 * hb + n32;
+            u32x2 w;
+            w[0] = pack_bf16x2(o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb]);
+            w[1] = pack_bf16x2(o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]);
+            *(u32x2 LDS_AS*)(sm + hh * kStride + col * 2) = w;
+          }
+      __syncthreads();
+      uint8_t* orow = (uint8_t*)a.out + (size_t)tile * a.H * kDimV * 2;
+      for (int e = tid; e < nrows * 64; e += 256) {      // 64 x 16 B per head row
+        const int hh = e >> 6, c16 = e & 63;
+        *(u32x4*)(orow + (size_t)hh * 1024 + c16 * 16) = *(const u32x4 LDS_AS*)(sm + hh * kStride + c16 * 16);
+      }
+    } else {
+      // fp32 partial rows [head][512], two rounds of 64 heads, stride 2064 B
+      constexpr int kStride = 2064;
+      float* prow = a.ws.part_out + (size_t)slot * a.H * kDimV;
+#pragma unroll
+      for (int round = 0; round < 2; ++round) {
+#pragma unroll
+        for (int cbl = 0; cbl < 4; ++cbl)
+#pragma unroll
+          for (int hbr = 0; hbr < 2; ++hbr)
 #pragma unroll
             for (int rg = 0; rg < 4; ++rg) {
-              const int col = 32 * cb + 8 * rg + 4 * h;
-              f32x4 w = {o[cb][4 * rg] * inv, o[cb][4 * rg + 1] * inv, o[cb][4 * rg + 2] * inv,
-                         o[cb][4 * rg + 3] * inv};
-              *(f32x4*)(prow + col) = w;
+              const int hb = 2 * round + hbr;
+              const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
+              const int hh = 32 * hbr + n32;  // row within this round
+              const f32x4 w = {o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb],
+                               o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]};
+              *(f32x4 LDS_AS*)(sm + hh * kStride + col * 4) = w;
             }
-          if (h == 0) a.ws.part_lse[(size_t)slot * a.H + head] = lse_nat;
+        __syncthreads();
+        const int rows = min(64, nrows - 64 * round);
+        for (int e = tid; e < rows * 128; e += 256) {   // 128 x 16 B per head row
+          const int hh = e >> 7, c16 = e & 127;
+          *(u32x4*)(prow + (size_t)(64 * round + hh) * kDimV + c16 * 4) =
+              *(const u32x4 LDS_AS*)(sm + hh * kStride + c16 * 16);
         }
+        __syncthreads();
       }
     }
   }
