@@ -63,6 +63,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="extra steps, each after a 1 GiB write that evicts L2 and MALL (reported separately)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -122,6 +124,21 @@ def main():
     combine_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
     step_ms = np.array([e[0].elapsed_time(e[3]) for e in events])
 
+    # Cold pass: the cache hierarchy (L2 + 256 MB MALL) is flushed before each
+    # step by writing a 1 GiB buffer outside the events.
+    cold = None
+    if args.cold_steps > 0:
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.cold_steps)]
+        for k in range(args.cold_steps):
+            scratch.fill_(k & 0xFF)
+            step(cev[k])
+        torch.cuda.synchronize()
+        del scratch
+        cold = {"steps": args.cold_steps,
+                "step_us_median": round(float(np.median([e[0].elapsed_time(e[3]) for e in cev])) * 1e3, 2),
+                "attend_us_median": round(float(np.median([e[1].elapsed_time(e[2]) for e in cev])) * 1e3, 2)}
+
     offs, _ = B.workspace_offsets(batch.B, batch.q_chunk, batch.H, 0)
     hdr = ws[offs[0]:offs[0] + 32].cpu().numpy().view(np.int32)
 
@@ -172,6 +189,8 @@ def main():
                  "split_tiles": int(hdr[6]), "workers": B.device_workers()},
         "roofline": roof,
     }
+    if cold is not None:
+        result["cold_cache"] = cold
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
