@@ -28,6 +28,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kernels.hpp"
 #include "splash_common.hpp"
 
@@ -139,6 +141,8 @@ constexpr int kPlanLdsTiles = 8192;  // tile page counts cached in LDS up to thi
 
 __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ int32_t s_pages[kPlanLdsTiles];
+  __shared__ int32_t s_ufirst[kPlanLdsTiles + 1];  // first unit of each tile (cached case)
+  __shared__ int32_t s_sfirst[kPlanLdsTiles];      // first partial slot of each tile (cached case)
   __shared__ int64_t s_red64[16];
   __shared__ int32_t s_red32[16];
   __shared__ int64_t s_cost[kNumCandidates + 1];
@@ -172,27 +176,49 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   const int32_t max_pages = mx > 0 ? mx : 1;
 
   // 2. unit size: evaluate every candidate (and a forced size), take the argmin.
-  for (int k = wave; k <= kNumCandidates; k += 16) {
-    int32_t c;
-    if (k < kNumCandidates) {
-      c = plan_candidate(k, max_pages);
-    } else {
-      if (p.forced_chunk <= 0) { if (lane == 0) { s_cost[k] = INT64_MAX; s_cand[k] = 0; } continue; }
-      c = p.forced_chunk < kMaxUnitPages ? p.forced_chunk : kMaxUnitPages;
+  // Wave w takes candidates w, w + 16, ...; one pass over the tiles counts
+  // units and split units for all of them, and one batched butterfly reduces
+  // the counts (independent shuffles overlap their latency).
+  {
+    constexpr int kPer = (kNumCandidates + 1 + 15) / 16;  // candidates per wave
+    int32_t cand[kPer];
+    int64_t Wc[kPer], Sc[kPer];
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) {
+      const int k = wave + 16 * m;
+      int32_t c = 0;
+      if (k < kNumCandidates) c = plan_candidate(k, max_pages);
+      else if (k == kNumCandidates && p.forced_chunk > 0) c = p.forced_chunk < kMaxUnitPages ? p.forced_chunk : kMaxUnitPages;
+      cand[m] = c;
+      Wc[m] = 0;
+      Sc[m] = 0;
     }
-    int64_t W = 0, S = 0;
     for (int32_t t = lane; t < T; t += 64) {
       const int32_t P = pages_of(t);
-      const int32_t n = P > 0 ? ceil_div(P, c) : 0;
-      W += n;
-      S += n > 1 ? n : 0;
+#pragma unroll
+      for (int m = 0; m < kPer; ++m) {
+        const int32_t n = (P > 0 && cand[m] > 0) ? ceil_div(P, cand[m]) : 0;
+        Wc[m] += n;
+        Sc[m] += n > 1 ? n : 0;
+      }
     }
-    W = wave_sum(W);
-    S = wave_sum(S);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+#pragma unroll
+      for (int m = 0; m < kPer; ++m) {
+        Wc[m] += __shfl_xor(Wc[m], o, 64);
+        Sc[m] += __shfl_xor(Sc[m], o, 64);
+      }
+    }
     if (lane == 0) {
-      const bool ok = S <= p.ws.max_partials && W <= p.ws.max_units;
-      s_cost[k] = ok ? plan_cost(c, W, S, total_pages, max_pages, p.G, kPlanCosts) : INT64_MAX;
-      s_cand[k] = c;
+#pragma unroll
+      for (int m = 0; m < kPer; ++m) {
+        const int k = wave + 16 * m;
+        if (k > kNumCandidates) continue;
+        const bool ok = cand[m] > 0 && Sc[m] <= p.ws.max_partials && Wc[m] <= p.ws.max_units;
+        s_cost[k] = ok ? plan_cost(cand[m], Wc[m], Sc[m], total_pages, max_pages, p.G, kPlanCosts) : INT64_MAX;
+        s_cand[k] = cand[m];
+      }
     }
   }
   __syncthreads();
@@ -229,13 +255,18 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     const int32_t es = block_exclusive_scan(sp, s_scan, &ts) + carry_s;
     const int32_t ef = block_exclusive_scan(f, s_scan, &tf) + carry_f;
     if (t < T) {
-      for (int32_t u = 0; u < n && eu + u < p.ws.max_units; ++u) {
-        int4 rec;
-        rec.x = t;
-        rec.y = unit_begin(P, n, u);
-        rec.z = unit_begin(P, n, u + 1);
-        rec.w = n > 1 ? es + u : -1;
-        p.ws.units[eu + u] = rec;
+      if (cached) {
+        s_ufirst[t] = eu;
+        s_sfirst[t] = es;
+      } else {
+        for (int32_t u = 0; u < n && eu + u < p.ws.max_units; ++u) {
+          int4 rec;
+          rec.x = t;
+          rec.y = unit_begin(P, n, u);
+          rec.z = unit_begin(P, n, u + 1);
+          rec.w = n > 1 ? es + u : -1;
+          p.ws.units[eu + u] = rec;
+        }
       }
       p.ws.indptr[t] = es < p.ws.max_partials ? es : p.ws.max_partials;
       if (f) p.ws.split_list[ef] = t;
@@ -243,6 +274,30 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     carry_u += tu;
     carry_s += ts;
     carry_f += tf;
+  }
+  // 4. unit records, one thread per unit (cached case): find the tile by
+  // binary search over the first-unit offsets.
+  if (cached) {
+    if (tid == 0) s_ufirst[T] = carry_u;
+    __syncthreads();
+    const int32_t U = carry_u < p.ws.max_units ? carry_u : p.ws.max_units;
+    for (int32_t ug = tid; ug < U; ug += 1024) {
+      int32_t lo = 0, hi = T - 1;  // last tile with s_ufirst[t] <= ug
+      while (lo < hi) {
+        const int32_t mid = (lo + hi + 1) >> 1;
+        if (s_ufirst[mid] <= ug) lo = mid; else hi = mid - 1;
+      }
+      const int32_t t = lo, u = ug - s_ufirst[t];
+      const int32_t P = s_pages[t];
+      const int32_t n = s_ufirst[t + 1] - s_ufirst[t];
+      const int32_t es = s_sfirst[t];
+      int4 rec;
+      rec.x = t;
+      rec.y = unit_begin(P, n, u);
+      rec.z = unit_begin(P, n, u + 1);
+      rec.w = n > 1 ? es + u : -1;
+      p.ws.units[ug] = rec;
+    }
   }
   if (tid == 0) {
     p.ws.indptr[T] = carry_s;
@@ -279,36 +334,40 @@ struct StepLayout {
   static constexpr int kGroupStride = kStepKeys * kGroupBytes;       // 2048 / 4096
   static constexpr int kData = kStepKeys * kRowBytes;                // 18432 / 36864
   static constexpr int kBuf = FP8 ? kData + 256 : kData;             // + fp32 scales
-  static constexpr int kBufs = 4;
+  // Ring slots: the step being multiplied (QK), the previous one (PV), and
+  // kDist steps in flight.
+  static constexpr int kSlots = FP8 ? 4 : 3;
+  static constexpr int kDist = kSlots - 2;
   static constexpr int kLoadsPerStep = FP8 ? 5 : 9;                  // per wave
-  static constexpr int kRing = kBufs * kBuf;
+  static constexpr int kRing = kSlots * kBuf;
 };
 
 // LDS map beyond the ring (bytes)
 constexpr int kPBytes = kMaxHeads * kStepKeys * 2;   // P for all heads, bf16
-constexpr int kRingMax = 4 * 36864;
 
 // Direct global->LDS loads, issued through asm so that the compiler's wait
 // insertion (which cannot tell which LDS bytes they write) does not drain
 // them before every LDS read; the kernel waits for them explicitly.  The
-// LDS destination is M0 + 16 * lane (4 * lane for the dword form); M0 is
-// restored afterwards.
-__device__ __forceinline__ void dma_b128(const void* gptr, const uint8_t LDS_AS* lds) {
+// source is a uniform 64-bit base plus a per-lane 32-bit offset; the LDS
+// destination is M0 + 16 * lane (4 * lane for the dword form).  No
+// instruction offset is used: it would move the LDS destination as well.
+// M0 is restored afterwards.
+__device__ __forceinline__ void dma_b128(const void* sbase, uint32_t voff, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
   asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(gptr), "s"(m0)
+      : "v"(voff), "s"(sbase), "s"(m0)
       : "memory");
 }
-__device__ __forceinline__ void dma_b32(const void* gptr, const uint8_t LDS_AS* lds) {
+__device__ __forceinline__ void dma_b32(const void* sbase, uint32_t voff, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
   asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2\n\ts_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(gptr), "s"(m0)
+      : "v"(voff), "s"(sbase), "s"(m0)
       : "memory");
 }
 
@@ -316,25 +375,36 @@ __device__ __forceinline__ void dma_b32(const void* gptr, const uint8_t LDS_AS* 
 //  bf16: wave w loads rows [8w, 8w+8) of every line group g (t = g);
 //  fp8:  instruction i = w + 4t (< 18) loads line group i >> 1, rows
 //        [16 (i & 1), +16); waves 2 and 3 also load the 32 token scales.
-// src_lane is the lane's byte offset inside the step for t = 0.
+// step_src / step_scales are uniform; src_lane is the lane's byte offset
+// inside the step for t = 0.
+template <bool FP8, int t>
+__device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
+                                          uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
+  if constexpr (!FP8) {
+    dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 1024 * wave);
+  } else {
+    if (t < 4 || wave + 4 * t < 18) {
+      dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+    } else {
+      const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+      dma_b32(step_scales, 4 * (lane & 31), buf + 18432);
+    }
+  }
+}
+
+template <bool FP8, int t = 0>
+__device__ __forceinline__ void issue_from(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
+                                           uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
+  if constexpr (t < StepLayout<FP8>::kLoadsPerStep) {
+    issue_one<FP8, t>(step_src, step_scales, src_lane, buf, wave);
+    issue_from<FP8, t + 1>(step_src, step_scales, src_lane, buf, wave);
+  }
+}
+
 template <bool FP8>
 __device__ __forceinline__ void issue_step(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                            uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
-  if constexpr (!FP8) {
-#pragma unroll
-    for (int t = 0; t < 9; ++t) dma_b128(step_src + src_lane + 128 * t, buf + 4096 * t + 1024 * wave);
-  } else {
-#pragma unroll
-    for (int t = 0; t < 5; ++t) {
-      const int i = wave + 4 * t;
-      if (t < 4 || i < 18) {
-        dma_b128(step_src + src_lane + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
-      } else {
-        const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
-        dma_b32(step_scales + (lane & 31), buf + 18432);
-      }
-    }
-  }
+  issue_from<FP8>(step_src, step_scales, src_lane, buf, wave);
 }
 
 // QK^T MFMAs are issued through inline asm with a VGPR accumulator: the
@@ -394,14 +464,81 @@ __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t ha
   return hh * 64 + (((2 * kh + half) ^ ((hh >> 2) & 3)) * 16);
 }
 
+// One 32-key step of the MFMA stream of a wave: its share of QK^T of step j
+// (when QK) interleaved with its share of PV of step j-1 (when PV).  The two
+// products are independent, so alternating them keeps the matrix pipe fed
+// while operand reads wait on LDS and dependent accumulations on each other.
+//  QK: the wave's query rows are two head blocks (qf[0], qf[1]) over the
+//      dims half dh (18 k-steps); each K fragment feeds both blocks: 36 MFMAs
+//      into sa (block of qf[0]) and sb (block of qf[1]), partial sums over
+//      half the dims.
+//  PV: 32 MFMAs, o[cbl][hb] += V^T(cb = 4*wave + cbl, kh) P^T(hb, kh) with
+//      V from `vbuf` and P from the P exchange area.
+template <bool FP8, bool QK, bool PV>
+__device__ __forceinline__ void mfma_stream(const uint8_t LDS_AS* kbuf, const uint32_t* kbase,
+                                            const bf16x8 (*qf)[18], f32x16& sa, f32x16& sb,
+                                            const uint8_t LDS_AS* vbuf, const uint32_t (*vbase)[2],
+                                            const uint8_t LDS_AS* p_lds, int wave, int n32, int h,
+                                            f32x16 (&o)[4][4]) {
+  constexpr int kKPre = 4;  // K fragments in flight
+  bf16x8 kf[kKPre];
+  if constexpr (QK) {
+#pragma unroll
+    for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(kbuf, kbase, ks);
+  }
+  // V fragments are double-buffered one column block ahead (c = 4kh + cbl).
+  bf16x8 pf[4], vf[2];
+  if constexpr (PV) {
+#pragma unroll
+    for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 0, h));
+    vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
+  }
+  constexpr int kIters = QK ? 36 : 32;
+  bf16x8 ka;
+#pragma unroll
+  for (int i = 0; i < kIters; ++i) {
+    if constexpr (PV) {
+      // prefetch the V fragment of the next column block before the MFMAs
+      // of this one
+      if (i < 32 && (i & 3) == 0 && i < 28) {
+        const int cn = (i >> 2) + 1;
+        vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+      }
+    }
+    if constexpr (QK) {
+      const int ks = i >> 1;
+      if ((i & 1) == 0) {
+        ka = kf[ks % kKPre];
+        if (ks + kKPre < 18) kf[ks % kKPre] = load_k_frag<FP8>(kbuf, kbase, ks + kKPre);
+        if (ks == 0) mfma_qk<true, FP8>(sa, ka, qf[0][ks]);
+        else mfma_qk<false, FP8>(sa, ka, qf[0][ks]);
+      } else {
+        if (ks == 0) mfma_qk<true, false>(sb, ka, qf[1][ks]);
+        else mfma_qk<false, false>(sb, ka, qf[1][ks]);
+      }
+    }
+    if constexpr (PV) {
+      if (i < 32) {
+        const int c = i >> 2, kh = i >> 4, cbl = (i >> 2) & 3, hb = i & 3;
+        o[cbl][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[cbl][hb], 0, 0, 0);
+        // P fragments of key half 1 replace those of half 0 once the last
+        // MFMA of half 0 that reads them has been issued
+        if (kh == 0 && cbl == 3)
+          pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 1, h));
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 template <bool FP8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   using L = StepLayout<FP8>;
-  constexpr int kStage = 128 * 1040 > 64 * 2064 ? 128 * 1040 : 64 * 2064;  // epilogue staging
-  constexpr int kPOff = L::kRing > kStage ? L::kRing : kStage;
-  constexpr int kLOff = kPOff + kPBytes;            // per-head normaliser, 128 floats
-  constexpr int kBtOff = kLOff + kMaxHeads * 4;     // block-table slice
+  constexpr int kPOff = L::kRing;                    // P exchange area, two steps
+  constexpr int kSOff = kPOff + 2 * kPBytes;         // partial-score exchange, 4 KB per wave
+  constexpr int kLOff = kSOff + 4 * 4096;            // per-head normaliser, 128 floats
+  constexpr int kBtOff = kLOff + kMaxHeads * 4;      // block-table slice
   constexpr int kSmem = kBtOff + kMaxUnitPages * 4;
   static_assert(kSmem <= 163840 - 64, "LDS budget");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
@@ -411,7 +548,10 @@ void attend_kernel(AttendLaunch a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int h = lane >> 5, n32 = lane & 31;
-  const int head = wave * 32 + n32;                           // head of the QK/softmax role
+  // QK role: head pair hp (head blocks 2hp, 2hp+1), dims half dh; the wave
+  // finishes the scores and the softmax of block 2hp + dh.
+  const int hp = wave & 1, dh = wave >> 1;
+  const int head = (2 * hp + dh) * 32 + n32;                  // head of the softmax role
   const bool head_ok = head < a.H;
   const int32_t num_units = a.ws.header[kHdrUnits];
   if (tid == 0) s_restart = 0;
@@ -419,6 +559,7 @@ void attend_kernel(AttendLaunch a) {
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
   uint8_t LDS_AS* p_lds = sm + kPOff;
+  uint8_t LDS_AS* s_xchg = sm + kSOff;
   float LDS_AS* l_lds = (float LDS_AS*)(sm + kLOff);
   int32_t LDS_AS* s_bt = (int32_t LDS_AS*)(sm + kBtOff);
 
@@ -434,13 +575,16 @@ void attend_kernel(AttendLaunch a) {
     dma_slot = 2048 * (wave >> 1) + 1024 * (wave & 1) + 16 * lane;   // + 4096 t
   }
   // K operand: row n32, chunk 2ks + h (bf16) / 16-byte chunk ks, half h (fp8)
+  // of the global k-step ks = 18dh + ks'.  kbase[ks' & 3] + G * (ks' >> 2)
+  // addresses k-step ks' of this wave's dims half (G = line-group stride).
   uint32_t kbase[4];
 #pragma unroll
-  for (int r4 = 0; r4 < 4; ++r4) {
+  for (int m = 0; m < 4; ++m) {
+    const int r4 = (2 * dh + m) & 3, g = 4 * dh + ((2 * dh + m) >> 2);
     if constexpr (!FP8)
-      kbase[r4] = n32 * 128 + (((2 * r4 + h) ^ ((n32 >> 1) & 7)) * 16);
+      kbase[m] = n32 * 128 + (((2 * r4 + h) ^ ((n32 >> 1) & 7)) * 16) + 4096 * g;
     else
-      kbase[r4] = n32 * 64 + ((r4 ^ ((n32 >> 1) & 3)) * 16) + 8 * h;
+      kbase[m] = n32 * 64 + ((r4 ^ ((n32 >> 1) & 3)) * 16) + 8 * h + 2048 * g;
   }
   // V operand (transposing reads), see load_v_frag
   const int i16 = lane & 15, g16 = lane >> 4;
@@ -490,30 +634,42 @@ void attend_kernel(AttendLaunch a) {
     const int32_t* bt = a.block_table + (size_t)b * a.bt_stride + p0;
     for (int k = tid; k < p1 - p0; k += 256) s_bt[k] = bt[k];
 
-    // Query fragment: B operand, row = head, k = dims 16*ks + 8*h + [0, 8).
-    bf16x8 qf[36];
-    {
-      const int qhead = head_ok ? head : 0;  // in-bounds row for padding heads
-      const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)tile * a.H + qhead) * kDimQK + 8 * h;
+    // Query fragments: B operands, k = dims 288dh + 16ks + 8h + [0, 8); row =
+    // head 32*(2hp + dh) + n32 (i = 0, the block this wave finishes) or
+    // 32*(2hp + 1 - dh) + n32 (i = 1, the partner's block).
+    bf16x8 qf[2][18];
 #pragma unroll
-      for (int ks = 0; ks < 36; ++ks) {
+    for (int i = 0; i < 2; ++i) {
+      const int qh = 32 * (2 * hp + (dh ^ i)) + n32;
+      const bool ok = qh < a.H;
+      const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)tile * a.H + (ok ? qh : 0)) * kDimQK + 288 * dh + 8 * h;
+#pragma unroll
+      for (int ks = 0; ks < 18; ++ks) {
         u32x4 v = *(const u32x4*)(qrow + 16 * ks);
-        if (!head_ok) v = (u32x4){0, 0, 0, 0};
-        qf[ks] = __builtin_bit_cast(bf16x8, v);
+        if (!ok) v = (u32x4){0, 0, 0, 0};  // padding heads
+        qf[i][ks] = __builtin_bit_cast(bf16x8, v);
       }
     }
     __syncthreads();  // block-table slice visible
 
-    auto step_src = [&](int j) {
+    auto step_src = [&](int j, int phys) {
       const int key = key_begin + j * kStepKeys;
-      const int phys = s_bt[(key >> 6) - p0];
       return kv + (size_t)phys * (kPage * L::kRowBytes) + (size_t)((key >> 5) & 1) * L::kData;
     };
-    auto step_scales = [&](int j) -> const float* {
+    auto step_scales = [&](int j, int phys) -> const float* {
       if constexpr (!FP8) return nullptr;
       const int key = key_begin + j * kStepKeys;
-      const int phys = s_bt[(key >> 6) - p0];
       return a.kv_scales + (size_t)phys * kPage + ((key >> 5) & 1) * kStepKeys;
+    };
+    auto step_phys = [&](int j) {
+      return __builtin_amdgcn_readfirstlane(s_bt[((key_begin + j * kStepKeys) >> 6) - p0]);
+    };
+    // ring slot of step j; the offset is laundered so the compiler keeps one
+    // scalar per step instead of deriving per-lane induction variables
+    auto slot_buf = [&](int j) {
+      uint32_t off = (uint32_t)(j % L::kSlots) * L::kBuf;
+      asm volatile("" : "+s"(off));
+      return sm + off;
     };
 
     // Softmax reference: fixed at the first step's max (O is still zero
@@ -524,10 +680,15 @@ void attend_kernel(AttendLaunch a) {
     float m_init = -INFINITY;
     f32x16 o[4][4];  // [column block cb - 4*wave][head block]
     float m_ref, l_run, l_exact;
-    for (;;) {
+    for (int pass = 0;; ++pass) {
+      // Pipeline: step j is staged kDist steps ahead; iteration j runs QK of
+      // step j together with PV of step j-1, then the softmax of step j.
 #pragma unroll
-      for (int j = 0; j < 3; ++j)
-        if (j < nsteps) issue_step<FP8>(step_src(j), step_scales(j), src_lane, sm + j * L::kBuf, wave);
+      for (int j = 0; j < L::kDist; ++j)
+        if (j < nsteps) {
+          const int ph = step_phys(j);
+          issue_step<FP8>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
+        }
 
 #pragma unroll
       for (int x = 0; x < 4; ++x)
@@ -539,13 +700,24 @@ void attend_kernel(AttendLaunch a) {
       float m_seen = -INFINITY;
       bool over = false;
 
-      for (int j = 0; j < nsteps; ++j) {
+      // One pipeline iteration: staging wait, QK of step j (interleaved with
+      // PV of step j-1, key half 0, and the loads of step j + kDist), the
+      // partial-score exchange, then the softmax of step j interleaved with
+      // PV of step j-1, key half 1.
+      auto qk_softmax = [&](int j, auto with_pv) {
+        constexpr bool kPV = decltype(with_pv)::value;
+        uint8_t LDS_AS* buf = slot_buf(j);                     // step j
+        uint8_t LDS_AS* vbuf = slot_buf(j + L::kSlots - 1);    // step j-1
+        const uint8_t LDS_AS* p_prev = p_lds + kPBytes * ((j + 1) & 1);  // P of step j-1
         const int key0 = key_begin + j * kStepKeys;
         const int valid = key_end - key0;  // >= 1
-        if (j + 2 < nsteps) wait_vmcnt<2 * L::kLoadsPerStep>();
-        else if (j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
+        const bool pf_next = j + L::kDist < nsteps;
+        const int pf_phys = pf_next ? step_phys(j + L::kDist) : 0;
+        const uint8_t* pf_src = step_src(j + L::kDist, pf_phys);
+        const float* pf_scales = step_scales(j + L::kDist, pf_phys);
+        uint8_t LDS_AS* pf_buf = slot_buf(j + L::kDist);
+        if (L::kDist == 2 && j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
         else wait_vmcnt<0>();
-        uint8_t LDS_AS* buf = sm + (j & 3) * L::kBuf;
         if (valid < kStepKeys) {
           // rows past the history end: P is zero there, V must not be NaN
           const u32x4 z = {0, 0, 0, 0};
@@ -554,102 +726,189 @@ void attend_kernel(AttendLaunch a) {
             for (int t = 0; t < L::kLoadsPerStep; ++t)
               if (!FP8 || t < 4 || wave + 4 * t < 18) *(u32x4 LDS_AS*)(buf + dma_slot + 4096 * t) = z;
           }
+          // their token scales too (both waves that load the scales clear
+          // them after their own loads landed, so a zero is written last)
+          if constexpr (FP8) {
+            if (wave >= 2 && (int)(lane & 31) >= valid) *(float LDS_AS*)(buf + L::kData + 4 * lane) = 0.f;
+          }
         }
-        lds_barrier();  // step j staged; every wave is past step j-1
-        if (j + 3 < nsteps)
-          issue_step<FP8>(step_src(j + 3), step_scales(j + 3), src_lane, sm + ((j + 3) & 3) * L::kBuf, wave);
+        // step j staged; P of step j-1 visible; every wave is done with
+        // iteration j-1, so the slot of step j-2 is free
+        lds_barrier();
 
-        // ---- S^T = K Q^T (A = K rows from LDS, B = resident query fragment)
-        constexpr int kKPre = 4;
-        bf16x8 kf[kKPre];
+        // ---- stream 1: QK^T of step j (36 MFMAs, partial over the wave's
+        // dims half) with PV of step j-1 key half 0 (16 MFMAs) in between.
+        f32x16 sacc, give;
+        bf16x8 pf[4], vf[2];
+        {
+          constexpr int kKPre = 4;  // K fragments in flight
+          bf16x8 kf[kKPre];
 #pragma unroll
-        for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
-        f32x16 s0, s1;
+          for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
+          if constexpr (kPV) {
 #pragma unroll
-        for (int ks = 0; ks < 36; ++ks) {
-          const bf16x8 ka = kf[ks % kKPre];
-          if (ks + kKPre < 36) kf[ks % kKPre] = load_k_frag<FP8>(buf, kbase, ks + kKPre);
-          if (ks == 0) mfma_qk<true, FP8>(s0, ka, qf[ks]);
-          else if (ks == 1) mfma_qk<true, FP8>(s1, ka, qf[ks]);
-          else if (ks & 1) mfma_qk<false, FP8>(s1, ka, qf[ks]);
-          else mfma_qk<false, FP8>(s0, ka, qf[ks]);
+            for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 0, h));
+            vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
+          }
+          bf16x8 ka;
+#pragma unroll
+          for (int i = 0; i < 36; ++i) {
+            const int ks = i >> 1;
+            if constexpr (kPV) {
+              // V fragment of the next column block (c = 4kh + cbl), one ahead
+              if ((i & 3) == 0 && i < 16) {
+                const int cn = (i >> 2) + 1;
+                vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+              }
+            }
+            if ((i & 1) == 0) {
+              ka = kf[ks % kKPre];
+              if (ks + kKPre < 18) kf[ks % kKPre] = load_k_frag<FP8>(buf, kbase, ks + kKPre);
+              if (ks == 0) mfma_qk<true, FP8>(sacc, ka, qf[0][ks]);
+              else mfma_qk<false, FP8>(sacc, ka, qf[0][ks]);
+            } else {
+              if (ks == 0) mfma_qk<true, false>(give, ka, qf[1][ks]);
+              else mfma_qk<false, false>(give, ka, qf[1][ks]);
+            }
+            if constexpr (kPV) {
+              if (i < 16) {
+                const int c = i >> 2, hb = i & 3;
+                o[c][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[c][hb], 0, 0, 0);
+                // key half 1 P fragments replace half 0 after their last use
+                if (c == 3) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
+              }
+            }
+            // the loads of step j + kDist, spread over the stream
+            if ((i & 3) == 1 && (i >> 2) < L::kLoadsPerStep && pf_next) {
+              switch (i >> 2) {
+                case 0: issue_one<FP8, 0>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 1: issue_one<FP8, 1>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 2: issue_one<FP8, 2>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 3: issue_one<FP8, 3>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 4: issue_one<FP8, 4>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 5: issue_one<FP8, 5>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 6: issue_one<FP8, 6>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                case 7: issue_one<FP8, 7>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                default: issue_one<FP8, 8>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
-        wait_mfma_vgpr(s0, s1);
-        f32x16 sacc = s0 + s1;
+        wait_mfma_vgpr(sacc, give);
+        // hand the partner (same head pair, other dims half) its block
+        {
+          uint8_t LDS_AS* dst = s_xchg + (wave ^ 2) * 4096 + 16 * lane;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *(f32x4 LDS_AS*)(dst + 1024 * q) = (f32x4){give[4 * q], give[4 * q + 1], give[4 * q + 2], give[4 * q + 3]};
+        }
+        lds_barrier();  // partial scores exchanged
+        {
+          const uint8_t LDS_AS* src = s_xchg + wave * 4096 + 16 * lane;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 r = *(const f32x4 LDS_AS*)(src + 1024 * q);
+            sacc[4 * q] += r[0];
+            sacc[4 * q + 1] += r[1];
+            sacc[4 * q + 2] += r[2];
+            sacc[4 * q + 3] += r[3];
+          }
+        }
 
-        // ---- online softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3)
-        float mx = -INFINITY;
+        // ---- softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3).
+        // t = z*log2(e) - m_ref; the reference is set by the unit's first step.
+        f32x2 sc[8];
+        if constexpr (FP8) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = 8 * (r >> 2) + 4 * h + (r & 3);
-          float x = sacc[r] * c2;
-          if constexpr (FP8) x *= *(const float LDS_AS*)(buf + L::kData + 4 * m);
-          x = m < valid ? x : -INFINITY;
-          sacc[r] = x;
-          mx = fmaxf(mx, x);
+          for (int r = 0; r < 16; r += 2) {
+            const int m = 8 * (r >> 2) + 4 * h + (r & 3);
+            sc[r >> 1] = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * m);
+            sacc[r] *= sc[r >> 1][0];
+            sacc[r + 1] *= sc[r >> 1][1];
+          }
         }
-        mx = fmaxf(mx, wave_xor32(mx));
-        if (m_ref == -INFINITY) m_ref = mx;
-        m_seen = fmaxf(m_seen, mx);
-        over |= mx > m_ref + 64.0f;
+        if (valid < kStepKeys) {
+          // the last step of a history: keys past its end get no weight
+          const int hk = (int)opaque(4 * h);
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (hk + (8 * (r >> 2) + (r & 3)) >= valid) sacc[r] = -INFINITY;
+        }
+        if (m_ref == -INFINITY) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2);
+          m_ref = fmaxf(mx, wave_xor32(mx));
+        }
+        // ---- stream 2: the softmax (one element per MFMA slot) with PV of
+        // step j-1 key half 1 (16 MFMAs).
         // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
         // output by the sum of the rounded weights, so the weights applied to V
         // sum to one and only the spread of the rounding errors reaches the
         // output; the LSE keeps the exact fp32 sum.
-        float psum = 0.f, pexact = 0.f;
+        float psum = 0.f, pexact = 0.f, mt = -INFINITY, plo = 0.f;
         unsigned pb[8];
 #pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          float pa = __builtin_amdgcn_exp2f(sacc[r] - m_ref), pc = __builtin_amdgcn_exp2f(sacc[r + 1] - m_ref);
-          pexact += pa + pc;
-          if constexpr (FP8) {
-            const int ma = 8 * (r >> 2) + 4 * h + (r & 3);
-            const f32x2 sc2 = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * ma);
-            pa = ma < valid ? pa * sc2[0] : 0.f;
-            pc = ma + 1 < valid ? pc * sc2[1] : 0.f;
-            pb[r >> 1] = pack_bf16x2(pa, pc);
-          } else {
-            const unsigned w = pack_bf16x2(pa, pc);
-            pb[r >> 1] = w;
-            psum += __builtin_bit_cast(float, w << 16) + __builtin_bit_cast(float, w & 0xFFFF0000u);
+        for (int r = 0; r < 16; ++r) {
+          if constexpr (kPV) {
+            const int c = 4 + (r >> 2), hb = r & 3;
+            if ((r & 3) == 0 && c + 1 < 8) {
+              const int cn = c + 1;
+              vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+            }
+            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[c & 3][hb], 0, 0, 0);
           }
+          const float t = __builtin_fmaf(sacc[r], c2, -m_ref);
+          mt = fmaxf(mt, t);
+          const float p = __builtin_amdgcn_exp2f(t);
+          pexact += p;
+          if (r & 1) {
+            if constexpr (FP8) {
+              // the token scale multiplies V too: fold it into the weight
+              pb[r >> 1] = pack_bf16x2(plo * sc[r >> 1][0], p * sc[r >> 1][1]);
+            } else {
+              const unsigned w = pack_bf16x2(plo, p);
+              pb[r >> 1] = w;
+              psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), (bf16x2){1.0f, 1.0f}, psum, false);
+            }
+          } else {
+            plo = p;
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
+        mt = fmaxf(mt, wave_xor32(mt));
+        m_seen = fmaxf(m_seen, m_ref + mt);
+        over |= mt > 64.0f;
         l_exact += pexact;
         l_run += FP8 ? pexact : psum;
         // publish this wave's P^T (keys in slot order) for every wave's PV
-        *(u32x4 LDS_AS*)(p_lds + p_slot(head, 0, h)) = (u32x4){pb[0], pb[1], pb[2], pb[3]};
-        *(u32x4 LDS_AS*)(p_lds + p_slot(head, 1, h)) = (u32x4){pb[4], pb[5], pb[6], pb[7]};
-        lds_barrier();  // P of all heads visible
+        uint8_t LDS_AS* p_cur = p_lds + kPBytes * (j & 1);
+        *(u32x4 LDS_AS*)(p_cur + p_slot(head, 0, h)) = (u32x4){pb[0], pb[1], pb[2], pb[3]};
+        *(u32x4 LDS_AS*)(p_cur + p_slot(head, 1, h)) = (u32x4){pb[4], pb[5], pb[6], pb[7]};
+      };
 
-        // ---- O^T[cols of this wave, all heads] += V^T P^T
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh) {
-          bf16x8 pf[4];
-#pragma unroll
-          for (int hb = 0; hb < 4; ++hb)
-            pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, kh, h));
-          bf16x8 vf = load_v_frag<FP8>(buf, vbase, 4 * wave, kh);
-#pragma unroll
-          for (int cbl = 0; cbl < 4; ++cbl) {
-            const bf16x8 va = vf;
-            if (cbl < 3) vf = load_v_frag<FP8>(buf, vbase, 4 * wave + cbl + 1, kh);
-#pragma unroll
-            for (int hb = 0; hb < 4; ++hb)
-              o[cbl][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[hb], o[cbl][hb], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
+      qk_softmax(0, std::false_type{});
+      for (int j = 1; j < nsteps; ++j) qk_softmax(j, std::true_type{});
+      // PV of the last step
+      lds_barrier();
+      {
+        f32x16 sa, sb;
+        mfma_stream<FP8, false, true>(sm, kbase, qf, sa, sb, slot_buf(nsteps - 1), vbase,
+                                      p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o);
       }
       if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
       __syncthreads();
       const bool restart = s_restart != 0;
       __syncthreads();
-      if (!restart) break;
+      // the second pass starts from the unit's true max, so it never
+      // overflows; it is the last one in any case
+      if (!restart || pass > 0) break;
       if (tid == 0) s_restart = 0;
       m_init = m_seen;
     }  // pass
 
-    // ---- epilogue: normalise, stage through LDS, write whole rows
+    // ---- epilogue: normalise and store straight from the accumulators
     {
       // normaliser: sum of the weights as applied (rounded); LSE: exact sum
       const float l_tot = l_run + wave_xor32(l_run);
@@ -668,56 +927,41 @@ void attend_kernel(AttendLaunch a) {
     float inv[4];
 #pragma unroll
     for (int hb = 0; hb < 4; ++hb) inv[hb] = 1.f / l_lds[32 * hb + n32];
-    const int nrows = a.H;  // rows (heads) of this tile that exist
+    // lane: head 32hb + n32; 4 consecutive columns 32cb + 8rg + 4h + [0, 4)
     if (slot < 0) {
-      // bf16 [head][512] rows, stride 1040 B in LDS
-      constexpr int kStride = 1040;
-#pragma unroll
-      for (int cbl = 0; cbl < 4; ++cbl)
-#pragma unroll
-        for (int hb = 0; hb < 4; ++hb)
-#pragma unroll
-          for (int rg = 0; rg < 4; ++rg) {
-            const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
-            const int hh = 32 * hb + n32;
-            u32x2 w;
-            w[0] = pack_bf16x2(o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb]);
-            w[1] = pack_bf16x2(o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]);
-            *(u32x2 LDS_AS*)(sm + hh * kStride + col * 2) = w;
-          }
-      __syncthreads();
       uint8_t* orow = (uint8_t*)a.out + (size_t)tile * a.H * kDimV * 2;
-      for (int e = tid; e < nrows * 64; e += 256) {      // 64 x 16 B per head row
-        const int hh = e >> 6, c16 = e & 63;
-        *(u32x4*)(orow + (size_t)hh * 1024 + c16 * 16) = *(const u32x4 LDS_AS*)(sm + hh * kStride + c16 * 16);
-      }
-    } else {
-      // fp32 partial rows [head][512], two rounds of 64 heads, stride 2064 B
-      constexpr int kStride = 2064;
-      float* prow = a.ws.part_out + (size_t)slot * a.H * kDimV;
 #pragma unroll
-      for (int round = 0; round < 2; ++round) {
+      for (int hb = 0; hb < 4; ++hb) {
+        const int hh = 32 * hb + n32;
+        if (hh < a.H) {
 #pragma unroll
-        for (int cbl = 0; cbl < 4; ++cbl)
-#pragma unroll
-          for (int hbr = 0; hbr < 2; ++hbr)
+          for (int cbl = 0; cbl < 4; ++cbl)
 #pragma unroll
             for (int rg = 0; rg < 4; ++rg) {
-              const int hb = 2 * round + hbr;
               const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
-              const int hh = 32 * hbr + n32;  // row within this round
+              u32x2 w;
+              w[0] = pack_bf16x2(o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb]);
+              w[1] = pack_bf16x2(o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]);
+              *(u32x2*)(orow + (size_t)hh * (kDimV * 2) + col * 2) = w;
+            }
+        }
+      }
+    } else {
+      float* prow = a.ws.part_out + (size_t)slot * a.H * kDimV;
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb) {
+        const int hh = 32 * hb + n32;
+        if (hh < a.H) {
+#pragma unroll
+          for (int cbl = 0; cbl < 4; ++cbl)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+              const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
               const f32x4 w = {o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb],
                                o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]};
-              *(f32x4 LDS_AS*)(sm + hh * kStride + col * 4) = w;
+              *(f32x4*)(prow + (size_t)hh * kDimV + col) = w;
             }
-        __syncthreads();
-        const int rows = min(64, nrows - 64 * round);
-        for (int e = tid; e < rows * 128; e += 256) {   // 128 x 16 B per head row
-          const int hh = e >> 7, c16 = e & 127;
-          *(u32x4*)(prow + (size_t)(64 * round + hh) * kDimV + c16 * 4) =
-              *(const u32x4 LDS_AS*)(sm + hh * kStride + c16 * 16);
         }
-        __syncthreads();
       }
     }
   }

@@ -28,18 +28,21 @@ constexpr int kHeaderInts = 64;
 // L = s_b - q_chunk + i + 1 keys (its complete causal prefix), i.e.
 // ceil(L/64) pages.  The planner cuts each tile's page range into units of at
 // most c pages; a tile cut into more than one unit writes fp32 partials that
-// the combine step merges.  c is chosen by an argmin of an estimated
-// makespan over candidate sizes: the units of all tiles are list-scheduled
-// on G persistent workers, so the estimate is the mean load plus half the
-// largest unit, with a fixed cost per unit (query load, pipeline fill) and
-// per split unit (partial write + read back), in page equivalents.
+// the combine step merges.  c is chosen by an argmin of an estimated step
+// time over candidate sizes.  The G persistent workers take units from a
+// queue, so with W units the busiest worker runs R = ceil(W / G) of them: the
+// estimate is max(R * c, work / G) plus, per unit on that worker, a fixed
+// cost (query load, pipeline fill), per split unit on it the partial write,
+// and the combine's read of all S partials spread over the workers; all in
+// page equivalents, scaled by 16 G so the arithmetic is integral.
 
 struct PlanCosts {
-  int32_t unit_x16;   // per-unit overhead, pages * 16
-  int32_t split_x16;  // extra per unit of a split tile, pages * 16
+  int32_t unit_x16;     // per unit on the busiest worker, pages * 16
+  int32_t split_x16;    // per split unit on the busiest worker (partial write), pages * 16
+  int32_t combine_x16;  // per partial, spread over the workers (combine read), pages * 16
 };
 
-constexpr PlanCosts kPlanCosts = {40, 56};
+constexpr PlanCosts kPlanCosts = {16, 32, 48};
 constexpr int kNumCandidates = 96;
 
 SPLASH_HD int32_t tile_keys(int32_t seq_len, int32_t q_chunk, int32_t i) {
@@ -61,18 +64,22 @@ SPLASH_HD int32_t plan_candidate(int32_t k, int32_t max_pages) {
   return c < 1 ? 1 : c;
 }
 
-// Estimated makespan (page equivalents * 16) of unit size c, given the
+// Estimated step time of unit size c (page equivalents * 16 * G), given the
 // number of units W and split units S it produces.
 SPLASH_HD int64_t plan_cost(int32_t c, int64_t W, int64_t S, int64_t total_pages,
                             int32_t max_pages, int32_t G, PlanCosts k) {
-  int64_t work = total_pages * 16 + (int64_t)k.unit_x16 * W + (int64_t)k.split_x16 * S;
-  int32_t biggest = c < max_pages ? c : max_pages;
-  int64_t big = (int64_t)biggest * 16 + k.unit_x16 + (c < max_pages ? k.split_x16 : 0);
-  return work / G + big / 2;
+  const int64_t R = (W + G - 1) / G;                       // units on the busiest worker
+  const int64_t RS = (S + G - 1) / G;                      // split units on it, at most R
+  const int64_t c_eff = c < max_pages ? c : max_pages;
+  const int64_t busy = R * c_eff * 16 * G;
+  const int64_t mean = total_pages * 16;
+  return (busy > mean ? busy : mean) + R * k.unit_x16 * G + (RS < R ? RS : R) * k.split_x16 * G +
+         S * k.combine_x16;
 }
 
 // Unit u (0-based) of a tile of P pages cut into n units: [P*u/n, P*(u+1)/n).
 SPLASH_HD int32_t unit_begin(int32_t P, int32_t n, int32_t u) {
+  if (P < 46341) return (int32_t)(((uint32_t)P * (uint32_t)u) / (uint32_t)n);  // product fits in 31 bits
   return (int32_t)(((int64_t)P * u) / n);
 }
 

@@ -169,9 +169,17 @@ def test_host_plan_splits_few_long_and_balances():
     seq, spec = _lengths(3)
     d = B.make_desc(4, 128, 1882, 5640)
     units, _, stats = B.splash_mla_plan_host(seq, 1, d, 256, 0)
-    assert stats["units"] >= 256                    # enough work for every compute unit
+    assert stats["units"] >= 128                    # the four histories spread over the workers
     sizes = units[:, 2] - units[:, 1]
     assert sizes.max() <= 1.3 * stats["total_pages"] / 256 + 1
+
+
+def test_host_plan_keeps_many_short_requests_whole():
+    # one short history per worker: splitting would only add partial traffic
+    seq, spec = _lengths(2)
+    d = B.make_desc(256, 128, 64, int((-(-seq // 64)).sum()))
+    units, indptr, stats = B.splash_mla_plan_host(seq, 1, d, 256, 0)
+    assert stats["units"] == 256 and stats["partials"] == 0
 
 
 def test_host_plan_respects_partial_capacity_and_forced_split():
