@@ -95,6 +95,12 @@ __device__ __forceinline__ int32_t dev_tile_pages(const int32_t* seq_lens, int32
   return L > 0 ? ceil_div(L, kPage) : 0;
 }
 
+// Whole-wave reductions of the device library (DPP based, no LDS round trips).
+extern "C" __device__ __attribute__((const)) long long __ockl_wfred_add_i64(long long);
+extern "C" __device__ __attribute__((const)) long long __ockl_wfred_min_i64(long long);
+extern "C" __device__ __attribute__((const)) float __ockl_wfred_max_f32(float);
+extern "C" __device__ __attribute__((const)) float __ockl_wfred_add_f32(float);
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -109,24 +115,29 @@ __device__ __forceinline__ T wave_max(T v) {
   return v;
 }
 
+// Inclusive scan of one int per lane over the wave with DPP moves: prefix
+// sums inside each row of 16 lanes (shifts 1, 2, 4, 8), then the row totals
+// are broadcast into the following rows.
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15 -> rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31 -> rows 2, 3
+  return x;
+}
+
 // Exclusive block scan of one int per thread (1024 threads); returns the
 // exclusive prefix and writes the block total to *total.
 __device__ int32_t block_exclusive_scan(int32_t v, int32_t* wave_buf, int32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int32_t inc = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    int32_t n = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += n;
-  }
+  const int32_t inc = wave_incl_scan(v);
   if (lane == 63) wave_buf[wave] = inc;
   __syncthreads();
   if (wave == 0) {
     const int32_t x = lane < 16 ? wave_buf[lane] : 0;
-    int32_t run = x;
-    for (int o = 1; o < 16; o <<= 1) {
-      const int32_t n = __shfl_up(run, o, 64);
-      if (lane >= o) run += n;
-    }
+    const int32_t run = wave_incl_scan(x);
     if (lane < 16) wave_buf[lane] = run - x;
     if (lane == 15) wave_buf[16] = run;
   }
@@ -166,8 +177,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     tot += P;
     mx = P > mx ? P : mx;
   }
-  tot = wave_sum(tot);
-  mx = wave_max(mx);
+  tot = __ockl_wfred_add_i64(tot);
+  mx = __ockl_wfred_max_i32(mx);
   if (lane == 0) { s_red64[wave] = tot; s_red32[wave] = mx; }
   __syncthreads();
   tot = 0; mx = 0;
@@ -203,12 +214,9 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       }
     }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-#pragma unroll
-      for (int m = 0; m < kPer; ++m) {
-        Wc[m] += __shfl_xor(Wc[m], o, 64);
-        Sc[m] += __shfl_xor(Sc[m], o, 64);
-      }
+    for (int m = 0; m < kPer; ++m) {
+      Wc[m] = __ockl_wfred_add_i64(Wc[m]);
+      Sc[m] = __ockl_wfred_add_i64(Sc[m]);
     }
     if (lane == 0) {
 #pragma unroll
@@ -223,16 +231,15 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   }
   __syncthreads();
   if (wave == 0) {
-    // first minimum over the candidates (smallest index on ties)
+    // first minimum over the candidates (smallest index on ties): the key
+    // puts the cost above the candidate index (costs stay far below 2^56)
     int64_t best = INT64_MAX;
-    int bk = kNumCandidates;
-    for (int k = lane; k < kNumCandidates; k += 64)
-      if (s_cost[k] < best) { best = s_cost[k]; bk = k; }
-    for (int o = 32; o > 0; o >>= 1) {
-      const int64_t ob = __shfl_xor(best, o, 64);
-      const int ok = __shfl_xor(bk, o, 64);
-      if (ob < best || (ob == best && ok < bk)) { best = ob; bk = ok; }
+    for (int k = lane; k < kNumCandidates; k += 64) {
+      const int64_t key = s_cost[k] == INT64_MAX ? INT64_MAX : ((s_cost[k] << 7) | k);
+      best = key < best ? key : best;
     }
+    best = __ockl_wfred_min_i64(best);
+    int bk = best == INT64_MAX ? kNumCandidates : (int)(best & 127);
     if (lane == 0) {
       if (bk >= kNumCandidates) bk = 0;
       if (p.forced_chunk > 0 && s_cost[kNumCandidates] != INT64_MAX) bk = kNumCandidates;
@@ -978,70 +985,108 @@ void attend_kernel(AttendLaunch a) {
 }
 
 // ============================================================== combine ===
+
+constexpr int kCombineQuarters = 4;  // waves per (row, head): 128 columns each
 //
-// One wave per (request or tile, chunk row, head); 8 columns per lane.  The
-// LSE of all parts is reduced across the lanes first; then the partial rows
-// are summed with four parts' loads in flight.
+// Four wave slots per (request or tile, chunk row, head).  The LSE of all
+// parts is reduced across the lanes first.  With at most 8 parts the first
+// slot sums whole rows (8 columns per lane, every part's loads in flight at
+// once); with more, each slot sums 128 columns (2 per lane) with eight parts'
+// loads in flight.
 __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
   const int lane = threadIdx.x & 63;
   const int64_t wave_global = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  const int64_t per_req = (int64_t)c.q_chunk * c.H;
+  const int64_t per_req = (int64_t)c.q_chunk * c.H * kCombineQuarters;
   const int64_t nreq = c.item_list ? (int64_t)(*c.item_count) : (int64_t)c.B;
   for (int64_t item = wave_global; item < nreq * per_req; item += nwaves) {
     const int64_t ri = item / per_req;
     const int rem = (int)(item - ri * per_req);
-    const int qi = rem / c.H, hh = rem - qi * c.H;
+    const int quarter = rem & (kCombineQuarters - 1);
+    const int row = rem / kCombineQuarters;
+    const int qi = row / c.H, hh = row - qi * c.H;
     const int b = c.item_list ? c.item_list[ri] : (int)ri;
     const int s0 = c.indptr[b], s1 = c.indptr[b + 1];
     const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;
     if (s1 <= s0 && !c.write_empty) continue;
+    const int nparts = s1 - s0;
+    if (nparts <= 8 && quarter != 0) continue;  // the first slot takes the whole row
     const size_t stride = (size_t)c.q_chunk * c.H;           // between parts
     const size_t base = (size_t)qi * c.H + hh;
     const float* plse = c.partial_lse + base;
     float M = -INFINITY;
     for (int s = s0 + lane; s < s1; s += 64) M = fmaxf(M, plse[(size_t)s * stride]);
-    M = wave_max(M);
+    M = __ockl_wfred_max_f32(M);
     float wsum = 0.f;
     if (M > -INFINITY)
       for (int s = s0 + lane; s < s1; s += 64) wsum += __expf(plse[(size_t)s * stride] - M);
-    wsum = wave_sum(wsum);
-    f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-    if (M > -INFINITY) {
-      const float* prow = c.partials + base * kDimV + 8 * lane;
-      int s = s0;
-      for (; s + 4 <= s1; s += 4) {
-        f32x4 v[8];
-        float w[4];
+    wsum = __ockl_wfred_add_f32(wsum);
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    if (nparts <= 8) {
+      // few parts: the first wave of the row takes all 512 columns (8 per
+      // lane) and every part's loads are in flight at once
+      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+      if (M > -INFINITY) {
+        const float* prow = c.partials + base * kDimV + 8 * lane;
+        f32x4 v[16];
+        float w[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const f32x4* src = (const f32x4*)(prow + (size_t)(s + u) * stride * kDimV);
+        for (int u = 0; u < 8; ++u) {
+          const int su = s0 + (u < nparts ? u : nparts - 1);
+          const f32x4* src = (const f32x4*)(prow + (size_t)su * stride * kDimV);
           v[2 * u] = src[0];
           v[2 * u + 1] = src[1];
-          w[u] = plse[(size_t)(s + u) * stride];
+          w[u] = u < nparts ? plse[(size_t)su * stride] : -INFINITY;
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < 8; ++u) {
           const float wu = __expf(w[u] - M);
           acc0 += wu * v[2 * u];
           acc1 += wu * v[2 * u + 1];
         }
       }
-      for (; s < s1; ++s) {
-        const f32x4* src = (const f32x4*)(prow + (size_t)s * stride * kDimV);
-        const float wu = __expf(plse[(size_t)s * stride] - M);
-        acc0 += wu * src[0];
-        acc1 += wu * src[1];
+      u32x4 o4;
+      o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
+      o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
+      o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
+      o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
+      *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
+    } else {
+      // many parts: this wave's 128 columns, 2 per lane, 8 parts in flight
+      const int col = 128 * quarter + 2 * lane;
+      f32x2 acc = {0.f, 0.f};
+      if (M > -INFINITY) {
+        const float* prow = c.partials + base * kDimV + col;
+        constexpr int kU = 8;
+        int s = s0;
+        for (; s + kU <= s1; s += kU) {
+          f32x2 v[kU];
+          float w[kU];
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            v[u] = *(const f32x2*)(prow + (size_t)(s + u) * stride * kDimV);
+            w[u] = plse[(size_t)(s + u) * stride];
+          }
+#pragma unroll
+          for (int u = 0; u < kU; ++u) acc += __expf(w[u] - M) * v[u];
+        }
+        if (s < s1) {
+          // the remaining parts: independent loads, clamped to a valid part
+          f32x2 v[kU];
+          float w[kU];
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            const int su = s + u < s1 ? s + u : s1 - 1;
+            v[u] = *(const f32x2*)(prow + (size_t)su * stride * kDimV);
+            w[u] = s + u < s1 ? plse[(size_t)su * stride] : -INFINITY;
+          }
+#pragma unroll
+          for (int u = 0; u < kU; ++u) acc += __expf(w[u] - M) * v[u];
+        }
       }
+      *(unsigned*)((uint16_t*)c.out + orow * kDimV + col) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     }
-    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    u32x4 w;
-    w[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
-    w[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
-    w[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
-    w[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
-    *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = w;
-    if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+    if (lane == 0 && quarter == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
   }
 }
 
@@ -1105,9 +1150,9 @@ hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) 
 }
 
 hipError_t launch_combine(const CombineLaunch& c, hipStream_t s) {
-  int64_t items = (int64_t)c.B * c.q_chunk * c.H;
+  int64_t items = (int64_t)c.B * c.q_chunk * c.H * kCombineQuarters;
   int64_t blocks = (items + 3) / 4;
-  if (blocks > 2048) blocks = 2048;
+  if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(combine_kernel, dim3((unsigned)blocks), dim3(256), 0, s, c);
   return hipGetLastError();

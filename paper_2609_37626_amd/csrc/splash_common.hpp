@@ -51,6 +51,12 @@ SPLASH_HD int32_t tile_keys(int32_t seq_len, int32_t q_chunk, int32_t i) {
 
 SPLASH_HD int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
+// ceil(a / b) for a >= 0, b >= 1, with a 32-bit division whenever it fits.
+SPLASH_HD int64_t ceil_div_u(int64_t a, int32_t b) {
+  if (a < 0x7fffffffLL - b) return (int64_t)(((uint32_t)a + (uint32_t)b - 1u) / (uint32_t)b);
+  return (a + b - 1) / b;
+}
+
 // Candidate unit size k (0-based): ceil(maxP / (k+1)) for k < 64, then a
 // geometric continuation so very long tiles can be cut finely.
 SPLASH_HD int32_t plan_candidate(int32_t k, int32_t max_pages) {
@@ -68,8 +74,8 @@ SPLASH_HD int32_t plan_candidate(int32_t k, int32_t max_pages) {
 // number of units W and split units S it produces.
 SPLASH_HD int64_t plan_cost(int32_t c, int64_t W, int64_t S, int64_t total_pages,
                             int32_t max_pages, int32_t G, PlanCosts k) {
-  const int64_t R = (W + G - 1) / G;                       // units on the busiest worker
-  const int64_t RS = (S + G - 1) / G;                      // split units on it, at most R
+  const int64_t R = ceil_div_u(W, G);                      // units on the busiest worker
+  const int64_t RS = ceil_div_u(S, G);                     // split units on it, at most R
   const int64_t c_eff = c < max_pages ? c : max_pages;
   const int64_t busy = R * c_eff * 16 * G;
   const int64_t mean = total_pages * 16;
