@@ -704,9 +704,9 @@ void attend_kernel(AttendLaunch a) {
       m_ref = m_init;
       l_run = 0.f;
       l_exact = 0.f;
-      float m_seen = -INFINITY;
-      bool over = false;
+      float mt_max = -INFINITY;  // largest t = z*log2(e) - m_ref this pass, per lane
 
+      int next_phys = L::kDist < nsteps ? step_phys(L::kDist) : 0;
       // One pipeline iteration: staging wait, QK of step j (interleaved with
       // PV of step j-1, key half 0, and the loads of step j + kDist), the
       // partial-score exchange, then the softmax of step j interleaved with
@@ -719,7 +719,9 @@ void attend_kernel(AttendLaunch a) {
         const int key0 = key_begin + j * kStepKeys;
         const int valid = key_end - key0;  // >= 1
         const bool pf_next = j + L::kDist < nsteps;
-        const int pf_phys = pf_next ? step_phys(j + L::kDist) : 0;
+        const int pf_phys = next_phys;
+        // page of the step staged by the next iteration (LDS read, used then)
+        next_phys = j + L::kDist + 1 < nsteps ? step_phys(j + L::kDist + 1) : 0;
         const uint8_t* pf_src = step_src(j + L::kDist, pf_phys);
         const float* pf_scales = step_scales(j + L::kDist, pf_phys);
         uint8_t LDS_AS* pf_buf = slot_buf(j + L::kDist);
@@ -744,11 +746,14 @@ void attend_kernel(AttendLaunch a) {
         lds_barrier();
 
         // ---- stream 1: QK^T of step j (36 MFMAs, partial over the wave's
-        // dims half) with PV of step j-1 key half 0 (16 MFMAs) in between.
+        // dims half) with the first kPV1 MFMAs of PV of step j-1 in between
+        // (PV MFMA q: column block c = q >> 2 of key half c >> 2, head block
+        // q & 3); the other 32 - kPV1 run under the softmax (stream 2).
+        constexpr int kPV1 = 16;
         f32x16 sacc, give;
-        bf16x8 pf[4], vf[2];
+        bf16x8 pf[4], pf1[4], vf[3];
         {
-          constexpr int kKPre = 4;  // K fragments in flight
+          constexpr int kKPre = 3;  // K fragments in flight
           bf16x8 kf[kKPre];
 #pragma unroll
           for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
@@ -756,17 +761,21 @@ void attend_kernel(AttendLaunch a) {
 #pragma unroll
             for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 0, h));
             vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
+            vf[1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + 1, 0);
           }
           bf16x8 ka;
 #pragma unroll
           for (int i = 0; i < 36; ++i) {
             const int ks = i >> 1;
             if constexpr (kPV) {
-              // V fragment of the next column block (c = 4kh + cbl), one ahead
-              if ((i & 3) == 0 && i < 16) {
-                const int cn = (i >> 2) + 1;
-                vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+              // V fragment two column blocks ahead (c = 4kh + cbl)
+              if ((i & 3) == 0 && i < kPV1) {
+                const int cn = (i >> 2) + 2;
+                vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
               }
+              // key half 1 P fragments, well before stream 2 needs them
+              if (i >= kPV1 - 4 && i < kPV1)
+                pf1[i - kPV1 + 4] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * (i - kPV1 + 4) + n32, 1, h));
             }
             if ((i & 1) == 0) {
               ka = kf[ks % kKPre];
@@ -778,11 +787,9 @@ void attend_kernel(AttendLaunch a) {
               else mfma_qk<false, false>(give, ka, qf[1][ks]);
             }
             if constexpr (kPV) {
-              if (i < 16) {
+              if (i < kPV1) {
                 const int c = i >> 2, hb = i & 3;
-                o[c][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[c][hb], 0, 0, 0);
-                // key half 1 P fragments replace half 0 after their last use
-                if (c == 3) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
+                o[c][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pf[hb], o[c][hb], 0, 0, 0);
               }
             }
             // the loads of step j + kDist, spread over the stream
@@ -848,24 +855,15 @@ void attend_kernel(AttendLaunch a) {
           for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2);
           m_ref = fmaxf(mx, wave_xor32(mx));
         }
-        // ---- stream 2: the softmax (one element per MFMA slot) with PV of
-        // step j-1 key half 1 (16 MFMAs).
+        // ---- stream 2: the softmax (16 elements per lane) spread over the
+        // remaining PV MFMAs of step j-1.
         // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
         // output by the sum of the rounded weights, so the weights applied to V
         // sum to one and only the spread of the rounding errors reaches the
         // output; the LSE keeps the exact fp32 sum.
         float psum = 0.f, pexact = 0.f, mt = -INFINITY, plo = 0.f;
         unsigned pb[8];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if constexpr (kPV) {
-            const int c = 4 + (r >> 2), hb = r & 3;
-            if ((r & 3) == 0 && c + 1 < 8) {
-              const int cn = c + 1;
-              vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
-            }
-            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[c & 3][hb], 0, 0, 0);
-          }
+        auto softmax_elem = [&](int r) {
           const float t = __builtin_fmaf(sacc[r], c2, -m_ref);
           mt = fmaxf(mt, t);
           const float p = __builtin_amdgcn_exp2f(t);
@@ -882,11 +880,28 @@ void attend_kernel(AttendLaunch a) {
           } else {
             plo = p;
           }
+          // keep the element here, between the MFMAs of its slot, instead of
+          // letting the compiler sink the whole softmax below the stream
+          asm volatile("" : "+v"(pexact), "+v"(mt));
+        };
+        constexpr int kN2 = kPV ? 32 - kPV1 : 16;  // slots of stream 2
+#pragma unroll
+        for (int k = 0; k < kN2; ++k) {
+          if constexpr (kPV) {
+            const int q = kPV1 + k, c = q >> 2, hb = q & 3;
+            if (hb == 0 && c + 2 < 8) {
+              const int cn = c + 2;
+              vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+            }
+            const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
+            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+          }
+          // softmax elements of this slot: [ceil(16k / N2), ceil(16(k+1) / N2))
+#pragma unroll
+          for (int r = (16 * k + kN2 - 1) / kN2; r < (16 * (k + 1) + kN2 - 1) / kN2; ++r) softmax_elem(r);
           __builtin_amdgcn_sched_barrier(0);
         }
-        mt = fmaxf(mt, wave_xor32(mt));
-        m_seen = fmaxf(m_seen, m_ref + mt);
-        over |= mt > 64.0f;
+        mt_max = fmaxf(mt_max, mt);
         l_exact += pexact;
         l_run += FP8 ? pexact : psum;
         // publish this wave's P^T (keys in slot order) for every wave's PV
@@ -904,6 +919,9 @@ void attend_kernel(AttendLaunch a) {
         mfma_stream<FP8, false, true>(sm, kbase, qf, sa, sb, slot_buf(nsteps - 1), vbase,
                                       p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o);
       }
+      mt_max = fmaxf(mt_max, wave_xor32(mt_max));
+      const float m_seen = m_ref + mt_max;
+      const bool over = mt_max > 64.0f;
       if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
       __syncthreads();
       const bool restart = s_restart != 0;
