@@ -19,12 +19,45 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E
+KERNEL_SOURCES = ["paper_2609_37626_amd/csrc/kernels.hip", "paper_2609_37626_amd/csrc/splash_common.hpp",
+                  "paper_2609_37626_amd/csrc/kernels.hpp"]
 BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 METRIC = "us/step and achieved KV GB/s + MFMA TFLOP/s (% of roofline), paged MLA decode"
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per attend launch from the committed counter summary, if it
+    was taken on the kernel sources as they stand (else None)."""
+    path = os.path.join(ROOT, "profiles", "attend_kernel_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                fields.setdefault(k.strip(), []).append(v.strip())
+    digests = fields.get("kernel_source_sha256", [])
+    if not digests or digests[0] != kernel_source_digest():
+        return None
+    for w, fb, wb in zip(fields.get("workload", []), fields.get("fetch_bytes_per_launch", []),
+                         fields.get("write_bytes_per_launch", [])):
+        if w == workload:
+            return {"fetch_bytes": int(fb), "write_bytes": int(wb), "total_bytes": int(fb) + int(wb)}
+    return None
 
 
 def cpu_baseline(batch, budget_s):
@@ -155,6 +188,10 @@ def main():
         achieved = flops / attend_avg_s / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None}
+    traffic = measured_traffic(spec.name)
+    if traffic is not None:
+        roof["traffic"] = traffic["total_bytes"]
+        roof["traffic_detail"] = traffic
     roof.update({"kernel": "attend_kernel", "kernel_avg_us": round(attend_avg_s * 1e6, 2),
                  "alg_bytes_per_launch": int(alg_bytes), "alg_flops_per_launch": int(flops),
                  "roofline_us": round(max(hbm_time, mfma_time) * 1e6, 1)})
