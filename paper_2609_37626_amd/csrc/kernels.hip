@@ -706,7 +706,10 @@ void attend_kernel(AttendLaunch a) {
       l_exact = 0.f;
       float mt_max = -INFINITY;  // largest t = z*log2(e) - m_ref this pass, per lane
 
+      // page of the step staged next: read from LDS one iteration early, made
+      // uniform only where the loads are issued
       int next_phys = L::kDist < nsteps ? step_phys(L::kDist) : 0;
+      int next_phys_v = 0;
       // One pipeline iteration: staging wait, QK of step j (interleaved with
       // PV of step j-1, key half 0, and the loads of step j + kDist), the
       // partial-score exchange, then the softmax of step j interleaved with
@@ -719,9 +722,7 @@ void attend_kernel(AttendLaunch a) {
         const int key0 = key_begin + j * kStepKeys;
         const int valid = key_end - key0;  // >= 1
         const bool pf_next = j + L::kDist < nsteps;
-        const int pf_phys = next_phys;
-        // page of the step staged by the next iteration (LDS read, used then)
-        next_phys = j + L::kDist + 1 < nsteps ? step_phys(j + L::kDist + 1) : 0;
+        const int pf_phys = j == 0 ? next_phys : __builtin_amdgcn_readfirstlane(next_phys_v);
         const uint8_t* pf_src = step_src(j + L::kDist, pf_phys);
         const float* pf_scales = step_scales(j + L::kDist, pf_phys);
         uint8_t LDS_AS* pf_buf = slot_buf(j + L::kDist);
@@ -855,6 +856,8 @@ void attend_kernel(AttendLaunch a) {
           for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2);
           m_ref = fmaxf(mx, wave_xor32(mx));
         }
+        // page of the step the next iteration stages (read now, used there)
+        next_phys_v = j + L::kDist + 1 < nsteps ? s_bt[((key_begin + (j + L::kDist + 1) * kStepKeys) >> 6) - p0] : 0;
         // ---- stream 2: the softmax (16 elements per lane) spread over the
         // remaining PV MFMAs of step j-1.
         // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
@@ -896,9 +899,15 @@ void attend_kernel(AttendLaunch a) {
             const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
             o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
           }
-          // softmax elements of this slot: [ceil(16k / N2), ceil(16(k+1) / N2))
+          // softmax elements of this slot: [ceil(16k' / S), ceil(16(k'+1) / S))
+          // with k' = k - kLead over the S = N2 - kLead slots after the first
+          // kLead, which only issue MFMAs while the scores' LDS reads land
+          constexpr int kLead = kPV ? 3 : 0, kS = kN2 - kLead;
+          if (k >= kLead) {
+            const int kk = k - kLead;
 #pragma unroll
-          for (int r = (16 * k + kN2 - 1) / kN2; r < (16 * (k + 1) + kN2 - 1) / kN2; ++r) softmax_elem(r);
+            for (int r = (16 * kk + kS - 1) / kS; r < (16 * (kk + 1) + kS - 1) / kS; ++r) softmax_elem(r);
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
         mt_max = fmaxf(mt_max, mt);
