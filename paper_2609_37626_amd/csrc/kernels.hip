@@ -704,7 +704,7 @@ void attend_kernel(AttendLaunch a) {
       m_ref = m_init;
       l_run = 0.f;
       l_exact = 0.f;
-      float mt_max = -INFINITY;  // largest t = z*log2(e) - m_ref this pass, per lane
+      float zmax = -INFINITY;  // largest score of this pass, per lane
 
       // page of the step staged next: read from LDS one iteration early, made
       // uniform only where the loads are issued
@@ -774,9 +774,10 @@ void attend_kernel(AttendLaunch a) {
                 const int cn = (i >> 2) + 2;
                 vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
               }
-              // key half 1 P fragments, well before stream 2 needs them
-              if (i >= kPV1 - 4 && i < kPV1)
-                pf1[i - kPV1 + 4] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * (i - kPV1 + 4) + n32, 1, h));
+              // key half 1 P fragments, once the key half 0 ones are dead
+              // (they take their registers) and well before stream 2
+              if (i >= kPV1 && i < kPV1 + 4)
+                pf1[i - kPV1] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * (i - kPV1) + n32, 1, h));
             }
             if ((i & 1) == 0) {
               ka = kf[ks % kKPre];
@@ -811,6 +812,23 @@ void attend_kernel(AttendLaunch a) {
           }
         }
         wait_mfma_vgpr(sacc, give);
+        // PV MFMA q >= kPV1 of step j-1 (column block c = q >> 2, head block
+        // q & 3), with the V fragment of column block c + 2 loaded here
+        auto pv_slot = [&](int q) {
+          if constexpr (kPV) {
+            const int c = q >> 2, hb = q & 3;
+            if (hb == 0 && c + 2 < 8) {
+              const int cn = c + 2;
+              vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+            }
+            const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
+            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+          }
+        };
+        // kBridge PV MFMAs run through the exchange barrier, kLead more while
+        // the partner's scores are read back; the softmax rides on the rest
+        constexpr int kBridge = kPV ? 2 : 0, kLead = kPV ? 2 : 0;
+        constexpr int kN2 = kPV ? 32 - kPV1 - kBridge : 0;  // PV slots after the barrier
         // hand the partner (same head pair, other dims half) its block
         {
           uint8_t LDS_AS* dst = s_xchg + (wave ^ 2) * 4096 + 16 * lane;
@@ -818,60 +836,83 @@ void attend_kernel(AttendLaunch a) {
           for (int q = 0; q < 4; ++q)
             *(f32x4 LDS_AS*)(dst + 1024 * q) = (f32x4){give[4 * q], give[4 * q + 1], give[4 * q + 2], give[4 * q + 3]};
         }
+#pragma unroll
+        for (int k = 0; k < kBridge; ++k) {
+          pv_slot(kPV1 + k);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         lds_barrier();  // partial scores exchanged
+        f32x4 rx[4];
         {
           const uint8_t LDS_AS* src = s_xchg + wave * 4096 + 16 * lane;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4 r = *(const f32x4 LDS_AS*)(src + 1024 * q);
-            sacc[4 * q] += r[0];
-            sacc[4 * q + 1] += r[1];
-            sacc[4 * q + 2] += r[2];
-            sacc[4 * q + 3] += r[3];
-          }
+          for (int q = 0; q < 4; ++q) rx[q] = *(const f32x4 LDS_AS*)(src + 1024 * q);
         }
-
-        // ---- softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3).
-        // t = z*log2(e) - m_ref; the reference is set by the unit's first step.
         f32x2 sc[8];
         if constexpr (FP8) {
 #pragma unroll
           for (int r = 0; r < 16; r += 2) {
             const int m = 8 * (r >> 2) + 4 * h + (r & 3);
             sc[r >> 1] = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * m);
-            sacc[r] *= sc[r >> 1][0];
-            sacc[r + 1] *= sc[r >> 1][1];
           }
-        }
-        if (valid < kStepKeys) {
-          // the last step of a history: keys past its end get no weight
-          const int hk = (int)opaque(4 * h);
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (hk + (8 * (r >> 2) + (r & 3)) >= valid) sacc[r] = -INFINITY;
-        }
-        if (m_ref == -INFINITY) {
-          float mx = -INFINITY;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2);
-          m_ref = fmaxf(mx, wave_xor32(mx));
         }
         // page of the step the next iteration stages (read now, used there)
         next_phys_v = j + L::kDist + 1 < nsteps ? s_bt[((key_begin + (j + L::kDist + 1) * kStepKeys) >> 6) - p0] : 0;
+
+        // ---- full scores: own half plus the partner's, token scales (fp8),
+        // the history-end mask and, on the unit's first step, the reference.
+        // softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3);
+        // t = z*log2(e) - m_ref.
+        auto finish_scores = [&]() {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            sacc[4 * q] += rx[q][0];
+            sacc[4 * q + 1] += rx[q][1];
+            sacc[4 * q + 2] += rx[q][2];
+            sacc[4 * q + 3] += rx[q][3];
+          }
+          if constexpr (FP8) {
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+              sacc[r] *= sc[r >> 1][0];
+              sacc[r + 1] *= sc[r >> 1][1];
+            }
+          }
+          if (valid < kStepKeys) {
+            // the last step of a history: keys past its end get no weight
+            const int hk = (int)opaque(4 * h);
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if (hk + (8 * (r >> 2) + (r & 3)) >= valid) sacc[r] = -INFINITY;
+          }
+          if constexpr (!kPV) {
+            // first step of the pass: its largest score is the reference
+            // (a restarted pass already has one)
+            if (m_ref == -INFINITY) {
+              float mx = -INFINITY;
+#pragma unroll
+              for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2);
+              m_ref = fmaxf(mx, wave_xor32(mx));
+            }
+          }
+        };
+        if constexpr (!kPV) finish_scores();
+
         // ---- stream 2: the softmax (16 elements per lane) spread over the
         // remaining PV MFMAs of step j-1.
         // P is rounded to bf16 for the PV MFMA.  The bf16 path normalises the
         // output by the sum of the rounded weights, so the weights applied to V
         // sum to one and only the spread of the rounding errors reaches the
         // output; the LSE keeps the exact fp32 sum.
-        float psum = 0.f, pexact = 0.f, mt = -INFINITY, plo = 0.f;
+        float psum = 0.f, pexact = 0.f, plo = 0.f;
         unsigned pb[8];
         auto softmax_elem = [&](int r) {
           const float t = __builtin_fmaf(sacc[r], c2, -m_ref);
-          mt = fmaxf(mt, t);
           const float p = __builtin_amdgcn_exp2f(t);
           pexact += p;
           if (r & 1) {
+            // largest score of the pass (scaled for fp8), two per max3
+            zmax = fmaxf(zmax, fmaxf(sacc[r - 1], sacc[r]));
             if constexpr (FP8) {
               // the token scale multiplies V too: fold it into the weight
               pb[r >> 1] = pack_bf16x2(plo * sc[r >> 1][0], p * sc[r >> 1][1]);
@@ -885,32 +926,28 @@ void attend_kernel(AttendLaunch a) {
           }
           // keep the element here, between the MFMAs of its slot, instead of
           // letting the compiler sink the whole softmax below the stream
-          asm volatile("" : "+v"(pexact), "+v"(mt));
+          if constexpr (FP8) asm volatile("" : "+v"(pexact));
+          else asm volatile("" : "+v"(pexact), "+v"(psum));
         };
-        constexpr int kN2 = kPV ? 32 - kPV1 : 16;  // slots of stream 2
+        if constexpr (kPV) {
 #pragma unroll
-        for (int k = 0; k < kN2; ++k) {
-          if constexpr (kPV) {
-            const int q = kPV1 + k, c = q >> 2, hb = q & 3;
-            if (hb == 0 && c + 2 < 8) {
-              const int cn = c + 2;
-              vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+          for (int k = 0; k < kN2; ++k) {
+            pv_slot(kPV1 + kBridge + k);
+            if (k == kLead - 1) finish_scores();
+            // softmax elements of this slot: [ceil(16k' / S), ceil(16(k'+1) / S))
+            // with k' = k - kLead over the S = N2 - kLead slots after the lead
+            constexpr int kS = kN2 - kLead;
+            if (k >= kLead) {
+              const int kk = k - kLead;
+#pragma unroll
+              for (int r = (16 * kk + kS - 1) / kS; r < (16 * (kk + 1) + kS - 1) / kS; ++r) softmax_elem(r);
             }
-            const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
-            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
           }
-          // softmax elements of this slot: [ceil(16k' / S), ceil(16(k'+1) / S))
-          // with k' = k - kLead over the S = N2 - kLead slots after the first
-          // kLead, which only issue MFMAs while the scores' LDS reads land
-          constexpr int kLead = kPV ? 3 : 0, kS = kN2 - kLead;
-          if (k >= kLead) {
-            const int kk = k - kLead;
+        } else {
 #pragma unroll
-            for (int r = (16 * kk + kS - 1) / kS; r < (16 * (kk + 1) + kS - 1) / kS; ++r) softmax_elem(r);
-          }
-          __builtin_amdgcn_sched_barrier(0);
+          for (int r = 0; r < 16; ++r) softmax_elem(r);
         }
-        mt_max = fmaxf(mt_max, mt);
         l_exact += pexact;
         l_run += FP8 ? pexact : psum;
         // publish this wave's P^T (keys in slot order) for every wave's PV
@@ -928,7 +965,8 @@ void attend_kernel(AttendLaunch a) {
         mfma_stream<FP8, false, true>(sm, kbase, qf, sa, sb, slot_buf(nsteps - 1), vbase,
                                       p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o);
       }
-      mt_max = fmaxf(mt_max, wave_xor32(mt_max));
+      zmax = fmaxf(zmax, wave_xor32(zmax));
+      const float mt_max = __builtin_fmaf(zmax, c2, -m_ref);  // largest t of the pass
       const float m_seen = m_ref + mt_max;
       const bool over = mt_max > 64.0f;
       if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
