@@ -416,9 +416,10 @@ __device__ __forceinline__ void issue_step(const uint8_t* __restrict__ step_src,
 
 // QK^T MFMAs are issued through inline asm with a VGPR accumulator: the
 // compiler picks one MFMA destination class per function, and the output
-// accumulator already fills the 256 accumulation registers.  Two independent
-// chains alternate so no MFMA reads a result still in flight; wait_mfma_vgpr()
-// covers the latency before VALU code reads the chains.
+// accumulator already fills the 256 accumulation registers.  The QK^T of a
+// step is one accumulation chain: every MFMA adds into exactly the registers
+// the previous one wrote, which the matrix pipe forwards without wait states;
+// wait_mfma_vgpr() covers the latency before VALU code reads the result.
 template <bool FIRST, bool VALU_SRC>
 __device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& a, const bf16x8& b) {
   if constexpr (FIRST) {
@@ -434,8 +435,8 @@ __device__ __forceinline__ void mfma_qk(f32x16& acc, const bf16x8& a, const bf16
   }
 }
 
-__device__ __forceinline__ void wait_mfma_vgpr(f32x16& a0, f32x16& a1) {
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a0), "+v"(a1));
+__device__ __forceinline__ void wait_mfma_vgpr(f32x16& acc) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(acc));
 }
 
 // K operand fragment ks (A operand: lane = key row n32, 8 dims).
@@ -471,69 +472,32 @@ __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t ha
   return hh * 64 + (((2 * kh + half) ^ ((hh >> 2) & 3)) * 16);
 }
 
-// One 32-key step of the MFMA stream of a wave: its share of QK^T of step j
-// (when QK) interleaved with its share of PV of step j-1 (when PV).  The two
-// products are independent, so alternating them keeps the matrix pipe fed
-// while operand reads wait on LDS and dependent accumulations on each other.
-//  QK: the wave's query rows are two head blocks (qf[0], qf[1]) over the
-//      dims half dh (18 k-steps); each K fragment feeds both blocks: 36 MFMAs
-//      into sa (block of qf[0]) and sb (block of qf[1]), partial sums over
-//      half the dims.
-//  PV: 32 MFMAs, o[cbl][hb] += V^T(cb = 4*wave + cbl, kh) P^T(hb, kh) with
-//      V from `vbuf` and P from the P exchange area.
-template <bool FP8, bool QK, bool PV>
-__device__ __forceinline__ void mfma_stream(const uint8_t LDS_AS* kbuf, const uint32_t* kbase,
-                                            const bf16x8 (*qf)[18], f32x16& sa, f32x16& sb,
-                                            const uint8_t LDS_AS* vbuf, const uint32_t (*vbase)[2],
-                                            const uint8_t LDS_AS* p_lds, int wave, int n32, int h,
-                                            f32x16 (&o)[4][4]) {
-  constexpr int kKPre = 4;  // K fragments in flight
-  bf16x8 kf[kKPre];
-  if constexpr (QK) {
-#pragma unroll
-    for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(kbuf, kbase, ks);
-  }
+// PV of one 32-key step as a standalone MFMA stream (the unit's last step,
+// which has no QK to interleave with): 32 MFMAs,
+// o[cbl][hb] += V^T(cb = 4*wave + cbl, kh) P^T(hb, kh) with V from `vbuf` and
+// P from the P exchange area.
+template <bool FP8>
+__device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint32_t (*vbase)[2],
+                                          const uint8_t LDS_AS* p_lds, int wave, int n32, int h,
+                                          f32x16 (&o)[4][4]) {
   // V fragments are double-buffered one column block ahead (c = 4kh + cbl).
   bf16x8 pf[4], vf[2];
-  if constexpr (PV) {
 #pragma unroll
-    for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 0, h));
-    vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
-  }
-  constexpr int kIters = QK ? 36 : 32;
-  bf16x8 ka;
+  for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 0, h));
+  vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
 #pragma unroll
-  for (int i = 0; i < kIters; ++i) {
-    if constexpr (PV) {
-      // prefetch the V fragment of the next column block before the MFMAs
-      // of this one
-      if (i < 32 && (i & 3) == 0 && i < 28) {
-        const int cn = (i >> 2) + 1;
-        vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
-      }
+  for (int i = 0; i < 32; ++i) {
+    // prefetch the V fragment of the next column block before the MFMAs of
+    // this one
+    if ((i & 3) == 0 && i < 28) {
+      const int cn = (i >> 2) + 1;
+      vf[cn & 1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
     }
-    if constexpr (QK) {
-      const int ks = i >> 1;
-      if ((i & 1) == 0) {
-        ka = kf[ks % kKPre];
-        if (ks + kKPre < 18) kf[ks % kKPre] = load_k_frag<FP8>(kbuf, kbase, ks + kKPre);
-        if (ks == 0) mfma_qk<true, FP8>(sa, ka, qf[0][ks]);
-        else mfma_qk<false, FP8>(sa, ka, qf[0][ks]);
-      } else {
-        if (ks == 0) mfma_qk<true, false>(sb, ka, qf[1][ks]);
-        else mfma_qk<false, false>(sb, ka, qf[1][ks]);
-      }
-    }
-    if constexpr (PV) {
-      if (i < 32) {
-        const int c = i >> 2, kh = i >> 4, cbl = (i >> 2) & 3, hb = i & 3;
-        o[cbl][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[cbl][hb], 0, 0, 0);
-        // P fragments of key half 1 replace those of half 0 once the last
-        // MFMA of half 0 that reads them has been issued
-        if (kh == 0 && cbl == 3)
-          pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 1, h));
-      }
-    }
+    const int c = i >> 2, kh = i >> 4, cbl = (i >> 2) & 3, hb = i & 3;
+    o[cbl][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[cbl][hb], 0, 0, 0);
+    // P fragments of key half 1 replace those of half 0 once the last MFMA
+    // of half 0 that reads them has been issued
+    if (kh == 0 && cbl == 3) pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 1, h));
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -543,8 +507,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   using L = StepLayout<FP8>;
   constexpr int kPOff = L::kRing;                    // P exchange area, two steps
-  constexpr int kSOff = kPOff + 2 * kPBytes;         // partial-score exchange, 4 KB per wave
-  constexpr int kLOff = kSOff + 4 * 4096;            // per-head normaliser, 128 floats
+  constexpr int kLOff = kPOff + 2 * kPBytes;         // per-head normaliser, 128 floats
   constexpr int kBtOff = kLOff + kMaxHeads * 4;      // block-table slice
   constexpr int kSmem = kBtOff + kMaxUnitPages * 4;
   static_assert(kSmem <= 163840 - 64, "LDS budget");
@@ -555,10 +518,8 @@ void attend_kernel(AttendLaunch a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int h = lane >> 5, n32 = lane & 31;
-  // QK role: head pair hp (head blocks 2hp, 2hp+1), dims half dh; the wave
-  // finishes the scores and the softmax of block 2hp + dh.
-  const int hp = wave & 1, dh = wave >> 1;
-  const int head = (2 * hp + dh) * 32 + n32;                  // head of the softmax role
+  // QK and softmax role: head block `wave` (32 heads) over all 576 dims
+  const int head = 32 * wave + n32;
   const bool head_ok = head < a.H;
   const int32_t num_units = a.ws.header[kHdrUnits];
   if (tid == 0) s_restart = 0;
@@ -566,7 +527,6 @@ void attend_kernel(AttendLaunch a) {
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
   uint8_t LDS_AS* p_lds = sm + kPOff;
-  uint8_t LDS_AS* s_xchg = sm + kSOff;
   float LDS_AS* l_lds = (float LDS_AS*)(sm + kLOff);
   int32_t LDS_AS* s_bt = (int32_t LDS_AS*)(sm + kBtOff);
 
@@ -581,17 +541,16 @@ void attend_kernel(AttendLaunch a) {
     src_lane = dma_row * 576 + 64 * (wave >> 1) + (((lane & 3) ^ ((dma_row >> 1) & 3)) * 16);
     dma_slot = 2048 * (wave >> 1) + 1024 * (wave & 1) + 16 * lane;   // + 4096 t
   }
-  // K operand: row n32, chunk 2ks + h (bf16) / 16-byte chunk ks, half h (fp8)
-  // of the global k-step ks = 18dh + ks'.  kbase[ks' & 3] + G * (ks' >> 2)
-  // addresses k-step ks' of this wave's dims half (G = line-group stride).
+  // K operand of k-step ks (dims 16ks + 8h + [0, 8)): row n32, chunk
+  // 2(ks & 3) + h of line group ks >> 2 (bf16), or 16-byte chunk ks & 3, half
+  // h (fp8); kbase[ks & 3] + G * (ks >> 2) addresses it (G = group stride).
   uint32_t kbase[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    const int r4 = (2 * dh + m) & 3, g = 4 * dh + ((2 * dh + m) >> 2);
     if constexpr (!FP8)
-      kbase[m] = n32 * 128 + (((2 * r4 + h) ^ ((n32 >> 1) & 7)) * 16) + 4096 * g;
+      kbase[m] = n32 * 128 + (((2 * m + h) ^ ((n32 >> 1) & 7)) * 16);
     else
-      kbase[m] = n32 * 64 + ((r4 ^ ((n32 >> 1) & 3)) * 16) + 8 * h + 2048 * g;
+      kbase[m] = n32 * 64 + ((m ^ ((n32 >> 1) & 3)) * 16) + 8 * h;
   }
   // V operand (transposing reads), see load_v_frag
   const int i16 = lane & 15, g16 = lane >> 4;
@@ -641,20 +600,15 @@ void attend_kernel(AttendLaunch a) {
     const int32_t* bt = a.block_table + (size_t)b * a.bt_stride + p0;
     for (int k = tid; k < p1 - p0; k += 256) s_bt[k] = bt[k];
 
-    // Query fragments: B operands, k = dims 288dh + 16ks + 8h + [0, 8); row =
-    // head 32*(2hp + dh) + n32 (i = 0, the block this wave finishes) or
-    // 32*(2hp + 1 - dh) + n32 (i = 1, the partner's block).
-    bf16x8 qf[2][18];
+    // Query fragments: B operands, k = dims 16ks + 8h + [0, 8), row = head
+    bf16x8 qf[36];
+    {
+      const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)tile * a.H + (head_ok ? head : 0)) * kDimQK + 8 * h;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int qh = 32 * (2 * hp + (dh ^ i)) + n32;
-      const bool ok = qh < a.H;
-      const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)tile * a.H + (ok ? qh : 0)) * kDimQK + 288 * dh + 8 * h;
-#pragma unroll
-      for (int ks = 0; ks < 18; ++ks) {
+      for (int ks = 0; ks < 36; ++ks) {
         u32x4 v = *(const u32x4*)(qrow + 16 * ks);
-        if (!ok) v = (u32x4){0, 0, 0, 0};  // padding heads
-        qf[i][ks] = __builtin_bit_cast(bf16x8, v);
+        if (!head_ok) v = (u32x4){0, 0, 0, 0};  // padding heads
+        qf[ks] = __builtin_bit_cast(bf16x8, v);
       }
     }
     __syncthreads();  // block-table slice visible
@@ -704,16 +658,15 @@ void attend_kernel(AttendLaunch a) {
       m_ref = m_init;
       l_run = 0.f;
       l_exact = 0.f;
-      float zmax = -INFINITY;  // largest score of this pass, per lane
+      float tmax = -INFINITY;  // largest t = z*log2(e) - m_ref of this pass, per lane
 
       // page of the step staged next: read from LDS one iteration early, made
       // uniform only where the loads are issued
       int next_phys = L::kDist < nsteps ? step_phys(L::kDist) : 0;
       int next_phys_v = 0;
       // One pipeline iteration: staging wait, QK of step j (interleaved with
-      // PV of step j-1, key half 0, and the loads of step j + kDist), the
-      // partial-score exchange, then the softmax of step j interleaved with
-      // PV of step j-1, key half 1.
+      // half of PV of step j-1 and the loads of step j + kDist), then the
+      // softmax of step j interleaved with the other half of PV of step j-1.
       auto qk_softmax = [&](int j, auto with_pv) {
         constexpr bool kPV = decltype(with_pv)::value;
         uint8_t LDS_AS* buf = slot_buf(j);                     // step j
@@ -746,15 +699,16 @@ void attend_kernel(AttendLaunch a) {
         // iteration j-1, so the slot of step j-2 is free
         lds_barrier();
 
-        // ---- stream 1: QK^T of step j (36 MFMAs, partial over the wave's
-        // dims half) with the first kPV1 MFMAs of PV of step j-1 in between
-        // (PV MFMA q: column block c = q >> 2 of key half c >> 2, head block
-        // q & 3); the other 32 - kPV1 run under the softmax (stream 2).
-        constexpr int kPV1 = 16;
-        f32x16 sacc, give;
+        // ---- stream 1: QK^T of step j for the wave's head block (36 MFMAs,
+        // one K fragment each) with the first kPV1 MFMAs of PV of step j-1
+        // spread among them (PV MFMA q: column block c = q >> 2 of key half
+        // c >> 2, head block q & 3) and the loads of step j + kDist; the other
+        // 32 - kPV1 PV MFMAs run under the softmax (stream 2).
+        constexpr int kPV1 = 8;
+        f32x16 sacc;
         bf16x8 pf[4], pf1[4], vf[3];
         {
-          constexpr int kKPre = 3;  // K fragments in flight
+          constexpr int kKPre = 4;  // K fragments in flight
           bf16x8 kf[kKPre];
 #pragma unroll
           for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
@@ -764,35 +718,29 @@ void attend_kernel(AttendLaunch a) {
             vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
             vf[1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + 1, 0);
           }
-          bf16x8 ka;
 #pragma unroll
           for (int i = 0; i < 36; ++i) {
-            const int ks = i >> 1;
-            if constexpr (kPV) {
-              // V fragment two column blocks ahead (c = 4kh + cbl)
-              if ((i & 3) == 0 && i < kPV1) {
-                const int cn = (i >> 2) + 2;
-                vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
-              }
-              // key half 1 P fragments, once the key half 0 ones are dead
-              // (they take their registers) and well before stream 2
-              if (i >= kPV1 && i < kPV1 + 4)
-                pf1[i - kPV1] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * (i - kPV1) + n32, 1, h));
+            // PV MFMA q of this slot, if any: slot (36q) / kPV1
+            constexpr int kNone = -1;
+            const int qc = (i * kPV1 + 35) / 36;
+            const int q = (kPV && qc < kPV1 && (qc * 36) / kPV1 == i) ? qc : kNone;
+            if (q != kNone && (q & 3) == 0 && (q >> 2) + 2 < 8) {
+              // V fragment two column blocks ahead (c = 4kh + cbl); its ring
+              // entry last served column block c - 1
+              const int cn = (q >> 2) + 2;
+              vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
-            if ((i & 1) == 0) {
-              ka = kf[ks % kKPre];
-              if (ks + kKPre < 18) kf[ks % kKPre] = load_k_frag<FP8>(buf, kbase, ks + kKPre);
-              if (ks == 0) mfma_qk<true, FP8>(sacc, ka, qf[0][ks]);
-              else mfma_qk<false, FP8>(sacc, ka, qf[0][ks]);
-            } else {
-              if (ks == 0) mfma_qk<true, false>(give, ka, qf[1][ks]);
-              else mfma_qk<false, false>(give, ka, qf[1][ks]);
-            }
-            if constexpr (kPV) {
-              if (i < kPV1) {
-                const int c = i >> 2, hb = i & 3;
-                o[c][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pf[hb], o[c][hb], 0, 0, 0);
-              }
+            const bf16x8 ka = kf[i % kKPre];
+            if (i + kKPre < 36) kf[i % kKPre] = load_k_frag<FP8>(buf, kbase, i + kKPre);
+            if (i == 0) mfma_qk<true, FP8>(sacc, ka, qf[i]);
+            else mfma_qk<false, FP8>(sacc, ka, qf[i]);
+            if (q != kNone) {
+              const int c = q >> 2, hb = q & 3;
+              const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
+              o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+              // key half 1 P fragment of this head block, in the registers
+              // of the half 0 one, which column block 3 has just read last
+              if (c == 3) pf1[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
             }
             // the loads of step j + kDist, spread over the stream
             if ((i & 3) == 1 && (i >> 2) < L::kLoadsPerStep && pf_next) {
@@ -811,9 +759,8 @@ void attend_kernel(AttendLaunch a) {
             __builtin_amdgcn_sched_barrier(0);
           }
         }
-        wait_mfma_vgpr(sacc, give);
-        // PV MFMA q >= kPV1 of step j-1 (column block c = q >> 2, head block
-        // q & 3), with the V fragment of column block c + 2 loaded here
+        // PV MFMA q >= kPV1 of step j-1, with the V fragment of column block
+        // c + 2 loaded at the first MFMA of column block c
         auto pv_slot = [&](int q) {
           if constexpr (kPV) {
             const int c = q >> 2, hb = q & 3;
@@ -823,31 +770,16 @@ void attend_kernel(AttendLaunch a) {
             }
             const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
             o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+            // (as in stream 1) the key half 1 P fragment after the last read
+            // of the half 0 one
+            if (c == 3) pf1[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
           }
         };
-        // kBridge PV MFMAs run through the exchange barrier, kLead more while
-        // the partner's scores are read back; the softmax rides on the rest
-        constexpr int kBridge = kPV ? 2 : 0, kLead = kPV ? 2 : 0;
-        constexpr int kN2 = kPV ? 32 - kPV1 - kBridge : 0;  // PV slots after the barrier
-        // hand the partner (same head pair, other dims half) its block
-        {
-          uint8_t LDS_AS* dst = s_xchg + (wave ^ 2) * 4096 + 16 * lane;
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            *(f32x4 LDS_AS*)(dst + 1024 * q) = (f32x4){give[4 * q], give[4 * q + 1], give[4 * q + 2], give[4 * q + 3]};
-        }
-#pragma unroll
-        for (int k = 0; k < kBridge; ++k) {
-          pv_slot(kPV1 + k);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        lds_barrier();  // partial scores exchanged
-        f32x4 rx[4];
-        {
-          const uint8_t LDS_AS* src = s_xchg + wave * 4096 + 16 * lane;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) rx[q] = *(const f32x4 LDS_AS*)(src + 1024 * q);
-        }
+        // kLead PV MFMAs run while the QK chain drains, the last kTail after
+        // the P of step j is published (through the write and the next
+        // barrier); the softmax rides on the rest
+        constexpr int kLead = kPV ? 2 : 0, kTail = kPV ? 2 : 0;
+        constexpr int kN2 = kPV ? 32 - kPV1 - kTail : 0;  // PV slots of stream 2
         f32x2 sc[8];
         if constexpr (FP8) {
 #pragma unroll
@@ -859,18 +791,11 @@ void attend_kernel(AttendLaunch a) {
         // page of the step the next iteration stages (read now, used there)
         next_phys_v = j + L::kDist + 1 < nsteps ? s_bt[((key_begin + (j + L::kDist + 1) * kStepKeys) >> 6) - p0] : 0;
 
-        // ---- full scores: own half plus the partner's, token scales (fp8),
-        // the history-end mask and, on the unit's first step, the reference.
-        // softmax in base 2; lane = one head, keys 8(r>>2)+4h+(r&3);
-        // t = z*log2(e) - m_ref.
+        // ---- scores: token scales (fp8), the history-end mask and, on the
+        // unit's first step, the reference.  Softmax in base 2; lane = one
+        // head, keys 8(r>>2)+4h+(r&3); t = z*log2(e) - m_ref.
         auto finish_scores = [&]() {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            sacc[4 * q] += rx[q][0];
-            sacc[4 * q + 1] += rx[q][1];
-            sacc[4 * q + 2] += rx[q][2];
-            sacc[4 * q + 3] += rx[q][3];
-          }
+          wait_mfma_vgpr(sacc);
           if constexpr (FP8) {
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
@@ -904,15 +829,15 @@ void attend_kernel(AttendLaunch a) {
         // output by the sum of the rounded weights, so the weights applied to V
         // sum to one and only the spread of the rounding errors reaches the
         // output; the LSE keeps the exact fp32 sum.
-        float psum = 0.f, pexact = 0.f, plo = 0.f;
+        float psum = 0.f, pexact = 0.f, plo = 0.f, tlo = 0.f;
         unsigned pb[8];
         auto softmax_elem = [&](int r) {
           const float t = __builtin_fmaf(sacc[r], c2, -m_ref);
           const float p = __builtin_amdgcn_exp2f(t);
           pexact += p;
           if (r & 1) {
-            // largest score of the pass (scaled for fp8), two per max3
-            zmax = fmaxf(zmax, fmaxf(sacc[r - 1], sacc[r]));
+            // largest t of the pass, two per max3
+            tmax = fmaxf(tmax, fmaxf(tlo, t));
             if constexpr (FP8) {
               // the token scale multiplies V too: fold it into the weight
               pb[r >> 1] = pack_bf16x2(plo * sc[r >> 1][0], p * sc[r >> 1][1]);
@@ -923,6 +848,7 @@ void attend_kernel(AttendLaunch a) {
             }
           } else {
             plo = p;
+            tlo = t;
           }
           // keep the element here, between the MFMAs of its slot, instead of
           // letting the compiler sink the whole softmax below the stream
@@ -932,7 +858,7 @@ void attend_kernel(AttendLaunch a) {
         if constexpr (kPV) {
 #pragma unroll
           for (int k = 0; k < kN2; ++k) {
-            pv_slot(kPV1 + kBridge + k);
+            pv_slot(kPV1 + k);
             if (k == kLead - 1) finish_scores();
             // softmax elements of this slot: [ceil(16k' / S), ceil(16(k'+1) / S))
             // with k' = k - kLead over the S = N2 - kLead slots after the lead
@@ -954,19 +880,20 @@ void attend_kernel(AttendLaunch a) {
         uint8_t LDS_AS* p_cur = p_lds + kPBytes * (j & 1);
         *(u32x4 LDS_AS*)(p_cur + p_slot(head, 0, h)) = (u32x4){pb[0], pb[1], pb[2], pb[3]};
         *(u32x4 LDS_AS*)(p_cur + p_slot(head, 1, h)) = (u32x4){pb[4], pb[5], pb[6], pb[7]};
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < kTail; ++k) {
+          pv_slot(kPV1 + kN2 + k);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       };
 
       qk_softmax(0, std::false_type{});
       for (int j = 1; j < nsteps; ++j) qk_softmax(j, std::true_type{});
       // PV of the last step
       lds_barrier();
-      {
-        f32x16 sa, sb;
-        mfma_stream<FP8, false, true>(sm, kbase, qf, sa, sb, slot_buf(nsteps - 1), vbase,
-                                      p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o);
-      }
-      zmax = fmaxf(zmax, wave_xor32(zmax));
-      const float mt_max = __builtin_fmaf(zmax, c2, -m_ref);  // largest t of the pass
+      pv_stream<FP8>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o);
+      const float mt_max = fmaxf(tmax, wave_xor32(tmax));
       const float m_seen = m_ref + mt_max;
       const bool over = mt_max > 64.0f;
       if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
