@@ -157,7 +157,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ int64_t s_red64[16];
   __shared__ int32_t s_red32[16];
   __shared__ int64_t s_cost[kNumCandidates + 1];
+  __shared__ int64_t s_w[16][kNumCandidates + 1], s_s[16][kNumCandidates + 1];  // units, split units per tile slice
+  __shared__ int32_t s_list[kNumCandidates + 1];  // candidate index of each distinct size
+  __shared__ int32_t s_nd;                        // number of distinct sizes
+  __shared__ UDiv s_udiv[kNumCandidates + 1];      // their division magic
   __shared__ int32_t s_cand[kNumCandidates + 1];
+  __shared__ int32_t s_parts[kNumCandidates];  // parts of each candidate
   __shared__ int32_t s_scan[17];
   __shared__ int32_t s_chunk;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -177,6 +182,20 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     tot += P;
     mx = P > mx ? P : mx;
   }
+  // the candidates' part counts: k + 1 for k < 64, then the geometric
+  // recurrence of plan_candidate_parts (uniform, unrolled; lane i of wave 1
+  // keeps step i)
+  static_assert(kNumCandidates >= 64 && kNumCandidates - 64 <= 64, "candidate layout");
+  if (wave == 0) s_parts[lane] = lane + 1;
+  if (wave == 1) {
+    int32_t parts = 64, mine = 0;
+#pragma unroll
+    for (int i = 0; i < kNumCandidates - 64; ++i) {
+      parts += parts / 8;
+      if (lane == i) mine = parts;
+    }
+    if (lane < kNumCandidates - 64) s_parts[64 + lane] = mine;
+  }
   tot = __ockl_wfred_add_i64(tot);
   mx = __ockl_wfred_max_i32(mx);
   if (lane == 0) { s_red64[wave] = tot; s_red32[wave] = mx; }
@@ -187,55 +206,83 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   const int32_t max_pages = mx > 0 ? mx : 1;
 
   // 2. unit size: evaluate every candidate (and a forced size), take the argmin.
-  // Wave w takes candidates w, w + 16, ...; one pass over the tiles counts
-  // units and split units for all of them, and one batched butterfly reduces
-  // the counts (independent shuffles overlap their latency).
-  {
-    constexpr int kPer = (kNumCandidates + 1 + 15) / 16;  // candidates per wave
-    int32_t cand[kPer];
-    int64_t Wc[kPer], Sc[kPer];
+  // Wave 0 lists the distinct candidate sizes (a size equal to the previous
+  // candidate's is left out: the argmin keeps the smaller index on ties
+  // anyway).  Then every wave counts units and split units of listed
+  // candidates over a slice of the tiles: with at most 64 sizes lane j of
+  // wave w takes size j over the tiles t = w + 16i, otherwise sizes
+  // 64 (w >> 3) + j over t = (w & 7) + 8i.  The slices meet in LDS; wave 0
+  // adds them up, prices every size (one lane each) and takes the argmin.
+  if (wave == 0) {
+    int32_t nd = 0;
 #pragma unroll
-    for (int m = 0; m < kPer; ++m) {
-      const int k = wave + 16 * m;
-      int32_t c = 0;
-      if (k < kNumCandidates) c = plan_candidate(k, max_pages);
-      else if (k == kNumCandidates && p.forced_chunk > 0) c = p.forced_chunk < kMaxUnitPages ? p.forced_chunk : kMaxUnitPages;
-      cand[m] = c;
-      Wc[m] = 0;
-      Sc[m] = 0;
-    }
-    for (int32_t t = lane; t < T; t += 64) {
-      const int32_t P = pages_of(t);
-#pragma unroll
-      for (int m = 0; m < kPer; ++m) {
-        const int32_t n = (P > 0 && cand[m] > 0) ? ceil_div(P, cand[m]) : 0;
-        Wc[m] += n;
-        Sc[m] += n > 1 ? n : 0;
+    for (int r = 0; r < 2; ++r) {
+      const int k = 64 * r + lane;
+      int32_t ck = 0;
+      if (k < kNumCandidates) {
+        ck = plan_candidate_size(s_parts[k], max_pages);
+        if (k > 0 && plan_candidate_size(s_parts[k - 1], max_pages) == ck) ck = 0;
+      } else if (k == kNumCandidates && p.forced_chunk > 0) {
+        ck = p.forced_chunk < kMaxUnitPages ? p.forced_chunk : kMaxUnitPages;
       }
-    }
-#pragma unroll
-    for (int m = 0; m < kPer; ++m) {
-      Wc[m] = __ockl_wfred_add_i64(Wc[m]);
-      Sc[m] = __ockl_wfred_add_i64(Sc[m]);
+      if (k <= kNumCandidates) s_cand[k] = ck;
+      const uint64_t keep = __builtin_amdgcn_ballot_w64(ck > 0);
+      const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(keep >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)keep, 0));
+      if (ck > 0) {
+        s_list[nd + below] = k;
+        s_udiv[nd + below] = udiv_make((uint32_t)ck);  // once per size
+      }
+      nd += __builtin_popcountll(keep);
     }
     if (lane == 0) {
-#pragma unroll
-      for (int m = 0; m < kPer; ++m) {
-        const int k = wave + 16 * m;
-        if (k > kNumCandidates) continue;
-        const bool ok = cand[m] > 0 && Sc[m] <= p.ws.max_partials && Wc[m] <= p.ws.max_units;
-        s_cost[k] = ok ? plan_cost(cand[m], Wc[m], Sc[m], total_pages, max_pages, p.G, kPlanCosts) : INT64_MAX;
-        s_cand[k] = cand[m];
+      s_nd = nd;
+      s_cost[kNumCandidates] = INT64_MAX;
+    }
+  }
+  __syncthreads();
+  const int nd = s_nd;
+  const bool wide = nd > 64;
+  const int nsl = wide ? 8 : 16;  // tile slices
+  {
+    const int j = wide ? 64 * (wave >> 3) + lane : lane;
+    const int slice = wide ? (wave & 7) : wave;
+    if (j < nd) {
+      const int32_t ck = s_cand[s_list[j]];
+      const UDiv ud = s_udiv[j];
+      int64_t W = 0, S = 0;
+      auto count = [&](int32_t P) {
+        const int32_t n = (int32_t)udiv((uint32_t)(P + ck - 1), ud);  // ceil(P / c)
+        W += n;
+        S += n > 1 ? n : 0;
+      };
+      if (cached) {
+#pragma unroll 4
+        for (int32_t t = slice; t < T; t += nsl) count(s_pages[t]);
+      } else {
+        for (int32_t t = slice; t < T; t += nsl) count(dev_tile_pages(p.seq_lens, p.q_chunk, t));
       }
+      s_w[slice][j] = W;
+      s_s[slice][j] = S;
     }
   }
   __syncthreads();
   if (wave == 0) {
-    // first minimum over the candidates (smallest index on ties): the key
-    // puts the cost above the candidate index (costs stay far below 2^56)
+    // price every listed size (lane j, then j + 64), then the first minimum
+    // (smallest candidate index on ties): the key puts the cost above the
+    // candidate index (costs stay far below 2^56)
     int64_t best = INT64_MAX;
-    for (int k = lane; k < kNumCandidates; k += 64) {
-      const int64_t key = s_cost[k] == INT64_MAX ? INT64_MAX : ((s_cost[k] << 7) | k);
+    for (int j = lane; j < nd; j += 64) {
+      const int k = s_list[j];
+      const int32_t ck = s_cand[k];
+      int64_t W = 0, S = 0;
+      for (int sl = 0; sl < nsl; ++sl) {
+        W += s_w[sl][j];
+        S += s_s[sl][j];
+      }
+      const bool ok = S <= p.ws.max_partials && W <= p.ws.max_units;
+      const int64_t cost = ok ? plan_cost(ck, W, S, total_pages, max_pages, p.G, kPlanCosts) : INT64_MAX;
+      if (k == kNumCandidates) s_cost[kNumCandidates] = cost;
+      const int64_t key = (cost == INT64_MAX || k == kNumCandidates) ? INT64_MAX : ((cost << 7) | k);
       best = key < best ? key : best;
     }
     best = __ockl_wfred_min_i64(best);

@@ -51,23 +51,56 @@ SPLASH_HD int32_t tile_keys(int32_t seq_len, int32_t q_chunk, int32_t i) {
 
 SPLASH_HD int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
+// Division of 32-bit unsigned n by an invariant divisor 1 <= d <= 2^31 with
+// one multiply-high (Granlund and Montgomery, 1994; the round-up magic with
+// the extra add step): for 2^(l-1) < d <= 2^l, m = floor(2^32 (2^l - d) / d)
+// + 1 and t = mulhi(m, n) give floor(n / d) = (t + ((n - t) >> 1)) >> (l - 1)
+// for every 32-bit n.  d = 1 is passed through.
+struct UDiv {
+  uint32_t m, s, d;
+};
+SPLASH_HD UDiv udiv_make(uint32_t d) {
+  UDiv r;
+  r.d = d;
+  r.m = 0;
+  r.s = 0;
+  if (d >= 2) {
+    const uint32_t l = 32u - (uint32_t)__builtin_clz(d - 1u);  // ceil(log2 d)
+    r.m = (uint32_t)(((uint64_t)((1ull << l) - d) << 32) / d + 1u);
+    r.s = l - 1u;
+  }
+  return r;
+}
+SPLASH_HD uint32_t udiv(uint32_t n, UDiv v) {
+  const uint32_t t = (uint32_t)(((uint64_t)v.m * n) >> 32);
+  const uint32_t q = (t + ((n - t) >> 1)) >> v.s;
+  return v.d == 1u ? n : q;  // a select, no branch
+}
+
 // ceil(a / b) for a >= 0, b >= 1, with a 32-bit division whenever it fits.
 SPLASH_HD int64_t ceil_div_u(int64_t a, int32_t b) {
   if (a < 0x7fffffffLL - b) return (int64_t)(((uint32_t)a + (uint32_t)b - 1u) / (uint32_t)b);
   return (a + b - 1) / b;
 }
 
-// Candidate unit size k (0-based): ceil(maxP / (k+1)) for k < 64, then a
-// geometric continuation so very long tiles can be cut finely.
-SPLASH_HD int32_t plan_candidate(int32_t k, int32_t max_pages) {
+// Candidate unit size k (0-based): ceil(maxP / parts_k) with parts_k = k + 1
+// for k < 64, then a geometric continuation (parts_{k} = parts_{k-1} +
+// parts_{k-1} / 8 from parts_63 = 64) so very long tiles can be cut finely.
+SPLASH_HD int32_t plan_candidate_parts(int32_t k) {
   int32_t parts = k + 1;
   if (k >= 64) {
     parts = 64;
     for (int32_t j = 64; j <= k; ++j) parts += parts / 8;
   }
+  return parts;
+}
+SPLASH_HD int32_t plan_candidate_size(int32_t parts, int32_t max_pages) {
   int32_t c = ceil_div(max_pages, parts);
   if (c > kMaxUnitPages) c = kMaxUnitPages;
   return c < 1 ? 1 : c;
+}
+SPLASH_HD int32_t plan_candidate(int32_t k, int32_t max_pages) {
+  return plan_candidate_size(plan_candidate_parts(k), max_pages);
 }
 
 // Estimated step time of unit size c (page equivalents * 16 * G), given the

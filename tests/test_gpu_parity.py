@@ -192,22 +192,39 @@ def test_debug_gather_is_bit_exact():
         assert np.array_equal(dense.cpu().numpy(), want)
 
 
-def test_device_plan_matches_host_plan():
-    spec = W.CONFIGS[4]
-    rng = np.random.Generator(np.random.PCG64(spec.seed))
-    seq = W.draw_lengths(rng, spec)
-    d = B.make_desc(spec.B, spec.H, int(-(-seq.max() // 64)), int((-(-seq // 64)).sum()))
-    ws = torch.zeros(B.workspace_size(spec.B, 1, spec.H, 0), dtype=torch.uint8, device="cuda")
-    B.splash_mla_plan(torch.from_numpy(seq).cuda(), 1, d, ws)
+def _plan_lengths(case):
+    if case.startswith("cfg"):
+        spec = W.CONFIGS[int(case[3:])]
+        rng = np.random.Generator(np.random.PCG64(spec.seed))
+        return W.draw_lengths(rng, spec), spec.q_chunk, spec.H
+    lens = {
+        # one history long enough that the geometric candidates (index >= 64)
+        # are distinct sizes and can win
+        "one_long": [262144],
+        "long_and_short": [200000, 64, 65, 3000, 1],
+        "equal_lengths": [4096] * 40,
+    }[case]
+    return np.asarray(lens, dtype=np.int32), 1, 128
+
+
+@pytest.mark.parametrize("case", ["cfg2", "cfg3", "cfg4", "cfg5", "one_long", "long_and_short", "equal_lengths"])
+def test_device_plan_matches_host_plan(case):
+    seq, q_chunk, H = _plan_lengths(case)
+    Bn = len(seq)
+    d = B.make_desc(Bn, H, int(-(-seq.max() // 64)), int((-(-seq // 64)).sum()))
+    ws = torch.zeros(B.workspace_size(Bn, q_chunk, H, 0), dtype=torch.uint8, device="cuda")
+    B.splash_mla_plan(torch.from_numpy(seq).cuda(), q_chunk, d, ws)
     torch.cuda.synchronize()
-    units, indptr, stats = B.splash_mla_plan_host(seq, 1, d, B.device_workers(), 0)
-    offs, _ = B.workspace_offsets(spec.B, 1, spec.H, 0)
+    units, indptr, stats = B.splash_mla_plan_host(seq, q_chunk, d, B.device_workers(), 0)
+    offs, _ = B.workspace_offsets(Bn, q_chunk, H, 0)
     raw = ws.cpu().numpy()
     hdr = raw[offs[0]:offs[0] + 256].view(np.int32)
+    print(f"plan {case}: chunk {stats['chunk_pages']} units {stats['units']} partials {stats['partials']}", flush=True)
     assert hdr[1] == stats["units"] and hdr[2] == stats["partials"] and hdr[3] == stats["chunk_pages"]
     dev_units = raw[offs[1]:offs[1] + 16 * stats["units"]].view(np.int32).reshape(-1, 4)
     assert np.array_equal(dev_units, units)
-    dev_indptr = raw[offs[2]:offs[2] + 4 * (spec.B + 1)].view(np.int32)
+    T = Bn * q_chunk
+    dev_indptr = raw[offs[2]:offs[2] + 4 * (T + 1)].view(np.int32)
     assert np.array_equal(dev_indptr, indptr)
 
 
