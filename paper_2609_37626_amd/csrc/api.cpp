@@ -55,7 +55,7 @@ Layout layout_for(int64_t T, int32_t H, int64_t max_partials) {
   L.off[0] = o; o = align_up(o + sizeof(int32_t) * kHeaderInts);
   L.off[1] = o; o = align_up(o + 16 * (size_t)(T + max_partials));
   L.off[2] = o; o = align_up(o + sizeof(int32_t) * (size_t)(T + 1));
-  L.off[3] = o; o = align_up(o + sizeof(int32_t) * (size_t)(T > 0 ? T : 1));
+  L.off[3] = o; o = align_up(o + sizeof(int4) * (size_t)(T > 0 ? T : 1));
   L.off[4] = o; o = align_up(o + sizeof(float) * (size_t)max_partials * H);
   L.off[5] = o; o = align_up(o + sizeof(float) * (size_t)max_partials * H * kDimV);
   L.total = o;
@@ -80,7 +80,7 @@ Workspace workspace_view(void* ws, int64_t T, int32_t H, int64_t max_partials) {
   w.header = reinterpret_cast<int32_t*>(base + L.off[0]);
   w.units = reinterpret_cast<int4*>(base + L.off[1]);
   w.indptr = reinterpret_cast<int32_t*>(base + L.off[2]);
-  w.split_list = reinterpret_cast<int32_t*>(base + L.off[3]);
+  w.split_list = reinterpret_cast<int4*>(base + L.off[3]);
   w.part_lse = reinterpret_cast<float*>(base + L.off[4]);
   w.part_out = reinterpret_cast<float*>(base + L.off[5]);
   w.max_units = (int32_t)(T + max_partials);

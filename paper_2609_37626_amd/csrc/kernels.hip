@@ -323,7 +323,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
         }
       }
       p.ws.indptr[t] = es < p.ws.max_partials ? es : p.ws.max_partials;
-      if (f) p.ws.split_list[ef] = t;
+      if (f) {
+        // the same (clamped) range as indptr[t], indptr[t + 1]
+        const int32_t mp = p.ws.max_partials;
+        const int32_t r0 = es < mp ? es : mp, r1 = es + sp < mp ? es + sp : mp;
+        p.ws.split_list[ef] = make_int4(t, r0, r1 - r0, 0);
+      }
     }
     carry_u += tu;
     carry_s += ts;
@@ -1027,76 +1032,63 @@ void attend_kernel(AttendLaunch a) {
 
 constexpr int kCombineQuarters = 4;  // waves per (row, head): 128 columns each
 //
-// Four wave slots per (request or tile, chunk row, head).  The LSE of all
-// parts is reduced across the lanes first.  With at most 8 parts the first
-// slot sums whole rows (8 columns per lane, every part's loads in flight at
-// once); with more, each slot sums 128 columns (2 per lane) with eight parts'
-// loads in flight.
+// Four wave slots per (request or tile, chunk row, head), 128 columns each
+// (2 per lane).  With at most 8 parts every lane loads all parts' LSEs and
+// its columns of all parts at once; with more, the LSEs are reduced across
+// the lanes first and sixteen parts' columns are in flight at a time.
 __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
   const int lane = threadIdx.x & 63;
   const int64_t wave_global = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   const int64_t per_req = (int64_t)c.q_chunk * c.H * kCombineQuarters;
   const int64_t nreq = c.item_list ? (int64_t)(*c.item_count) : (int64_t)c.B;
-  for (int64_t item = wave_global; item < nreq * per_req; item += nwaves) {
-    const int64_t ri = item / per_req;
-    const int rem = (int)(item - ri * per_req);
-    const int quarter = rem & (kCombineQuarters - 1);
-    const int row = rem / kCombineQuarters;
-    const int qi = row / c.H, hh = row - qi * c.H;
-    const int b = c.item_list ? c.item_list[ri] : (int)ri;
-    const int s0 = c.indptr[b], s1 = c.indptr[b + 1];
+  const int64_t total = nreq * per_req;
+  const size_t stride = (size_t)c.q_chunk * c.H;  // between parts
+  // one (request or tile, row, head, quarter) item
+  auto combine_item = [&](int b, int s0, int s1, int quarter, int qi, int hh) {
     const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;
-    if (s1 <= s0 && !c.write_empty) continue;
     const int nparts = s1 - s0;
-    if (nparts <= 8 && quarter != 0) continue;  // the first slot takes the whole row
-    const size_t stride = (size_t)c.q_chunk * c.H;           // between parts
     const size_t base = (size_t)qi * c.H + hh;
     const float* plse = c.partial_lse + base;
-    float M = -INFINITY;
-    for (int s = s0 + lane; s < s1; s += 64) M = fmaxf(M, plse[(size_t)s * stride]);
-    M = __ockl_wfred_max_f32(M);
-    float wsum = 0.f;
-    if (M > -INFINITY)
-      for (int s = s0 + lane; s < s1; s += 64) wsum += __expf(plse[(size_t)s * stride] - M);
-    wsum = __ockl_wfred_add_f32(wsum);
-    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    const int col = 128 * quarter + 2 * lane;
+    float M = -INFINITY, wsum = 0.f;
+    f32x2 acc = {0.f, 0.f};
     if (nparts <= 8) {
-      // few parts: the first wave of the row takes all 512 columns (8 per
-      // lane) and every part's loads are in flight at once
-      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-      if (M > -INFINITY) {
-        const float* prow = c.partials + base * kDimV + 8 * lane;
-        f32x4 v[16];
-        float w[8];
+      // few parts: every lane loads every part's LSE itself (the same 32
+      // bytes for the whole wave) together with its 2 columns of every part,
+      // so the row costs one round trip to memory and no cross-lane reduction
+      const float* prow = c.partials + base * kDimV + col;
+      f32x2 v[8];
+      float w[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int su = s0 + (u < nparts ? u : nparts - 1);
-          const f32x4* src = (const f32x4*)(prow + (size_t)su * stride * kDimV);
-          v[2 * u] = src[0];
-          v[2 * u + 1] = src[1];
-          w[u] = u < nparts ? plse[(size_t)su * stride] : -INFINITY;
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const float wu = __expf(w[u] - M);
-          acc0 += wu * v[2 * u];
-          acc1 += wu * v[2 * u + 1];
+      for (int u = 0; u < 8; ++u) {
+        w[u] = -INFINITY;
+        v[u] = (f32x2){0.f, 0.f};
+        if (u < nparts) {  // uniform
+          w[u] = plse[(size_t)(s0 + u) * stride];
+          v[u] = *(const f32x2*)(prow + (size_t)(s0 + u) * stride * kDimV);
         }
       }
-      u32x4 o4;
-      o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
-      o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
-      o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
-      o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
-      *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) M = fmaxf(M, w[u]);
+      if (M > -INFINITY) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float wu = __expf(w[u] - M);  // 0 past the last part
+          wsum += wu;
+          acc += wu * v[u];
+        }
+      }
     } else {
-      // many parts: this wave's 128 columns, 2 per lane, 8 parts in flight
-      const int col = 128 * quarter + 2 * lane;
-      f32x2 acc = {0.f, 0.f};
+      for (int s = s0 + lane; s < s1; s += 64) M = fmaxf(M, plse[(size_t)s * stride]);
+      M = __ockl_wfred_max_f32(M);
+      if (M > -INFINITY)
+        for (int s = s0 + lane; s < s1; s += 64) wsum += __expf(plse[(size_t)s * stride] - M);
+      wsum = __ockl_wfred_add_f32(wsum);
+      // many parts: sixteen parts' columns in flight at a time
       if (M > -INFINITY) {
         const float* prow = c.partials + base * kDimV + col;
-        constexpr int kU = 8;
+        constexpr int kU = 16;
         int s = s0;
         for (; s + kU <= s1; s += kU) {
           f32x2 v[kU];
@@ -1123,9 +1115,32 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
           for (int u = 0; u < kU; ++u) acc += __expf(w[u] - M) * v[u];
         }
       }
-      *(unsigned*)((uint16_t*)c.out + orow * kDimV + col) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     }
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    *(unsigned*)((uint16_t*)c.out + orow * kDimV + col) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     if (lane == 0 && quarter == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+  };
+  for (int64_t item = wave_global; item < total; item += nwaves) {
+    const int64_t ri = item / per_req;
+    const int rem = (int)(item - ri * per_req);
+    const int quarter = rem & (kCombineQuarters - 1);
+    const int row = rem / kCombineQuarters;
+    const int qi = row / c.H, hh = row - qi * c.H;
+    // the request (or tile) and its part range: one record, or two reads of
+    // indptr
+    int b, s0, s1;
+    if (c.item_list) {
+      const int4 rec = c.item_list[ri];
+      b = rec.x;
+      s0 = rec.y;
+      s1 = rec.y + rec.z;
+    } else {
+      b = (int)ri;
+      s0 = c.indptr[b];
+      s1 = c.indptr[b + 1];
+    }
+    if (s1 <= s0 && !c.write_empty) continue;
+    combine_item(b, s0, s1, quarter, qi, hh);
   }
 }
 

@@ -12,7 +12,7 @@ struct Workspace {
   int32_t* header;      // kHeaderInts ints
   int4* units;          // [max_units]
   int32_t* indptr;      // [T + 1]
-  int32_t* split_list;  // [T] tiles that have partials (count in header[2]... see kernels)
+  int4* split_list;     // [T] {tile, first partial slot, parts, 0} of the tiles with partials (count in the header)
   float* part_lse;      // [max_partials, H]
   float* part_out;      // [max_partials, H, 512]
   int32_t max_units;
@@ -54,7 +54,8 @@ struct CombineLaunch {
   const float* partials;
   const float* partial_lse;
   const int32_t* indptr;     // [B + 1] partial-slot offsets (per request or per tile)
-  const int32_t* item_list;  // optional list of requests to process (count from *item_count)
+  const int4* item_list;     // optional {request, first slot, parts, 0} records to process (count from
+                             // *item_count); without it every request, with its range from indptr
   const int32_t* item_count;
   int32_t B, q_chunk, H;
   void* out;
