@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <climits>
 #include <cstdarg>
@@ -216,6 +217,7 @@ int do_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_d
   c.indptr = wv.indptr;
   c.item_list = wv.split_list;
   c.item_count = wv.header + kHdrSplitTiles;
+  c.max_parts = wv.header + kHdrMaxParts;
   c.B = d->batch * q_chunk;
   c.q_chunk = 1;
   c.H = d->num_heads;
@@ -358,6 +360,7 @@ int splash_mla_combine(const float* partials, const float* partial_lse, const in
   c.indptr = split_indptr;
   c.item_list = nullptr;
   c.item_count = nullptr;
+  c.max_parts = nullptr;
   c.B = batch;
   c.q_chunk = q_chunk;
   c.H = num_heads;
@@ -449,6 +452,18 @@ int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const sp
     ns += n > 1 ? n : 0;
   }
   if (T >= 0 && indptr_out) indptr_out[T] = ns;
+  if (T <= kPlanLdsTiles && nu > num_workers) {
+    // the device queue order: longest unit first (equal lengths in tile
+    // order here; the device leaves their order open)
+    std::vector<std::array<int32_t, 4>> rows((size_t)nu);
+    for (int32_t i = 0; i < nu; ++i)
+      for (int j = 0; j < 4; ++j) rows[i][j] = units_out[4 * (size_t)i + j];
+    std::stable_sort(rows.begin(), rows.end(), [](const std::array<int32_t, 4>& a, const std::array<int32_t, 4>& b) {
+      return a[2] - a[1] > b[2] - b[1];
+    });
+    for (int32_t i = 0; i < nu; ++i)
+      for (int j = 0; j < 4; ++j) units_out[4 * (size_t)i + j] = rows[i][j];
+  }
   if (stats_out) {
     stats_out[0] = nu;
     stats_out[1] = ns;

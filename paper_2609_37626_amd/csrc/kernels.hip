@@ -148,7 +148,6 @@ __device__ int32_t block_exclusive_scan(int32_t v, int32_t* wave_buf, int32_t* t
   return res;
 }
 
-constexpr int kPlanLdsTiles = 8192;  // tile page counts cached in LDS up to this many tiles
 
 __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ int32_t s_pages[kPlanLdsTiles];
@@ -163,6 +162,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ UDiv s_udiv[kNumCandidates + 1];      // their division magic
   __shared__ int32_t s_cand[kNumCandidates + 1];
   __shared__ int32_t s_parts[kNumCandidates];  // parts of each candidate
+  __shared__ int32_t s_lhist[kMaxUnitPages + 1];  // units per length
+  __shared__ int32_t s_lbase[kMaxUnitPages + 1];  // next queue slot per length
   __shared__ int32_t s_scan[17];
   __shared__ int32_t s_chunk;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -335,12 +336,18 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     carry_f += tf;
   }
   // 4. unit records, one thread per unit (cached case): find the tile by
-  // binary search over the first-unit offsets.
+  // binary search over the first-unit offsets.  With more units than workers
+  // the queue is ordered longest unit first (a counting sort over unit
+  // lengths; the order among units of equal length is whatever the LDS
+  // atomics give, and does not change any result), so the persistent workers
+  // pack the units the way a longest-processing-time-first schedule would.
+  // With at most one unit per worker every unit starts at once: tile order.
   if (cached) {
     if (tid == 0) s_ufirst[T] = carry_u;
+    for (int32_t i = tid; i <= kMaxUnitPages; i += 1024) s_lhist[i] = 0;
     __syncthreads();
     const int32_t U = carry_u < p.ws.max_units ? carry_u : p.ws.max_units;
-    for (int32_t ug = tid; ug < U; ug += 1024) {
+    auto unit_rec = [&](int32_t ug) {
       int32_t lo = 0, hi = T - 1;  // last tile with s_ufirst[t] <= ug
       while (lo < hi) {
         const int32_t mid = (lo + hi + 1) >> 1;
@@ -355,7 +362,27 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       rec.y = unit_begin(P, n, u);
       rec.z = unit_begin(P, n, u + 1);
       rec.w = n > 1 ? es + u : -1;
-      p.ws.units[ug] = rec;
+      return rec;
+    };
+    const bool lpt = U > p.G;  // uniform
+    for (int32_t ug = tid; ug < U; ug += 1024) {
+      const int4 rec = unit_rec(ug);
+      if (lpt) atomicAdd(&s_lhist[rec.z - rec.y], 1);  // 1 <= length <= kMaxUnitPages
+      else p.ws.units[ug] = rec;
+    }
+    __syncthreads();
+    if (lpt) {
+      // queue offset of each length: the number of longer units (thread i
+      // takes length kMaxUnitPages - i)
+      static_assert(kMaxUnitPages == 1024, "one thread per unit length");
+      const int32_t len = kMaxUnitPages - tid;
+      int32_t unused;
+      s_lbase[len] = block_exclusive_scan(s_lhist[len], s_scan, &unused);
+      __syncthreads();
+      for (int32_t ug = tid; ug < U; ug += 1024) {
+        const int4 rec = unit_rec(ug);
+        p.ws.units[atomicAdd(&s_lbase[rec.z - rec.y], 1)] = rec;
+      }
     }
   }
   if (tid == 0) {
@@ -367,6 +394,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     hdr[kHdrChunk] = c;
     hdr[kHdrSplitTiles] = carry_f;
     hdr[kHdrTotalPages] = total_pages > INT32_MAX ? INT32_MAX : (int32_t)total_pages;
+    hdr[kHdrMaxParts] = (max_pages + c - 1) / c;  // every tile has ceil(P / c) <= this many
   }
 }
 
@@ -1031,6 +1059,7 @@ void attend_kernel(AttendLaunch a) {
 // ============================================================== combine ===
 
 constexpr int kCombineQuarters = 4;  // waves per (row, head): 128 columns each
+constexpr int kCombineRowParts = 8;  // at most this many parts: one wave per (row, head)
 //
 // Four wave slots per (request or tile, chunk row, head), 128 columns each
 // (2 per lane).  With at most 8 parts every lane loads all parts' LSEs and
@@ -1043,7 +1072,61 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
   const int64_t per_req = (int64_t)c.q_chunk * c.H * kCombineQuarters;
   const int64_t nreq = c.item_list ? (int64_t)(*c.item_count) : (int64_t)c.B;
   const int64_t total = nreq * per_req;
+  if (total == 0) return;
   const size_t stride = (size_t)c.q_chunk * c.H;  // between parts
+  if (c.item_list && c.max_parts && *c.max_parts <= kCombineRowParts) {
+    // Every listed item has at most kCombineRowParts parts: one wave per
+    // (item, row, head) with 8 columns per lane, every part's LSE and columns
+    // loaded at once, so each row costs two round trips to memory (its record,
+    // then the data) and no cross-lane reduction.
+    const int64_t per_item = (int64_t)c.q_chunk * c.H;
+    for (int64_t item = wave_global; item < nreq * per_item; item += nwaves) {
+      const int64_t ri = item / per_item;
+      const int row = (int)(item - ri * per_item);
+      const int qi = row / c.H, hh = row - qi * c.H;
+      const int4 rec = c.item_list[ri];
+      const int b = rec.x, s0 = rec.y, np = rec.z;
+      const size_t base = (size_t)qi * c.H + hh;
+      const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;
+      const float* plse = c.partial_lse + base;
+      const float* prow = c.partials + base * kDimV + 8 * lane;
+      f32x4 v[kCombineRowParts][2];
+      float w[kCombineRowParts];
+#pragma unroll
+      for (int u = 0; u < kCombineRowParts; ++u) {
+        w[u] = -INFINITY;
+        v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        if (u < np) {  // uniform
+          w[u] = plse[(size_t)(s0 + u) * stride];
+          const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
+          v[u][0] = src[0];
+          v[u][1] = src[1];
+        }
+      }
+      float M = -INFINITY, wsum = 0.f;
+#pragma unroll
+      for (int u = 0; u < kCombineRowParts; ++u) M = fmaxf(M, w[u]);
+      f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+      if (M > -INFINITY) {
+#pragma unroll
+        for (int u = 0; u < kCombineRowParts; ++u) {
+          const float wu = __expf(w[u] - M);  // 0 past the last part
+          wsum += wu;
+          acc0 += wu * v[u][0];
+          acc1 += wu * v[u][1];
+        }
+      }
+      const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+      u32x4 o4;
+      o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
+      o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
+      o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
+      o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
+      *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
+      if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+    }
+    return;
+  }
   // one (request or tile, row, head, quarter) item
   auto combine_item = [&](int b, int s0, int s1, int quarter, int qi, int hh) {
     const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;

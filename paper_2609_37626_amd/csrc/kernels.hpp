@@ -29,6 +29,7 @@ enum HeaderSlot : int {
   kHdrDone = 5,        // workers that have drained the queue
   kHdrSplitTiles = 6,  // number of tiles with partials
   kHdrTotalPages = 7,
+  kHdrMaxParts = 8,    // upper bound on the parts of any split tile
 };
 
 struct PlanLaunch {
@@ -57,6 +58,7 @@ struct CombineLaunch {
   const int4* item_list;     // optional {request, first slot, parts, 0} records to process (count from
                              // *item_count); without it every request, with its range from indptr
   const int32_t* item_count;
+  const int32_t* max_parts;  // optional bound on the parts of every listed item
   int32_t B, q_chunk, H;
   void* out;
   float* out_lse;

@@ -21,6 +21,8 @@ constexpr int kMaxHeads = 128;
 constexpr int kStepKeys = 32;      // keys per pipeline step (half a page)
 constexpr int kMaxUnitPages = 1024;  // the block-table slice of one unit is staged in LDS
 constexpr int kHeaderInts = 64;
+constexpr int kPlanLdsTiles = 8192;  // planner: tile data cached in LDS, and the unit queue ordered longest
+                                     // first, up to this many tiles
 
 // ---------------------------------------------------------------- planner --
 //
@@ -110,10 +112,14 @@ SPLASH_HD int64_t plan_cost(int32_t c, int64_t W, int64_t S, int64_t total_pages
   const int64_t R = ceil_div_u(W, G);                      // units on the busiest worker
   const int64_t RS = ceil_div_u(S, G);                     // split units on it, at most R
   const int64_t c_eff = c < max_pages ? c : max_pages;
-  const int64_t busy = R * c_eff * 16 * G;
   const int64_t mean = total_pages * 16;
-  return (busy > mean ? busy : mean) + R * k.unit_x16 * G + (RS < R ? RS : R) * k.split_x16 * G +
-         S * k.combine_x16;
+  // Busiest worker: at most R units of at most c_eff pages, never below the
+  // mean.  (The queue hands out the longest units first; a finer estimate of
+  // that packing favoured splitting batches of short histories, but measured
+  // the saving did not cover the partial writes and the combine.)
+  int64_t busy = R * c_eff * 16 * G;
+  if (busy < mean) busy = mean;
+  return busy + R * k.unit_x16 * G + (RS < R ? RS : R) * k.split_x16 * G + S * k.combine_x16;
 }
 
 // Unit u (0-based) of a tile of P pages cut into n units: [P*u/n, P*(u+1)/n).

@@ -197,3 +197,25 @@ def test_host_plan_single_short_request_is_one_unit():
     d = B.make_desc(1, 16, 1, 1)
     units, indptr, stats = B.splash_mla_plan_host(np.array([1], np.int32), 1, d, 256, 0)
     assert units.tolist() == [[0, 0, 1, -1]] and indptr.tolist() == [0, 0]
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_host_plan_queue_order(cfg):
+    # the persistent workers take units in queue order.  With more units than
+    # workers the longest go first (ties in tile order), which packs them like
+    # a longest-processing-time-first schedule; with at most one unit per
+    # worker every unit starts at once and the queue stays in tile order.
+    seq, spec = _lengths(cfg)
+    d = B.make_desc(spec.B, spec.H, int(-(-seq.max() // 64)), int((-(-seq // 64)).sum()), spec.kv_dtype)
+    if spec.kv_dtype:
+        d.kv_scales = FAKE
+    units, indptr, stats = B.splash_mla_plan_host(seq, spec.q_chunk, d, 256, 0)
+    key = units[:, 0].astype(np.int64) * (1 << 32) + units[:, 1]
+    ln = units[:, 2] - units[:, 1]
+    if stats["units"] > 256:
+        assert np.all(ln[:-1] >= ln[1:])
+        same = ln[:-1] == ln[1:]
+        assert np.all(key[:-1][same] < key[1:][same])
+    else:
+        assert np.all(key[:-1] < key[1:])
+    check_plan(seq, spec.q_chunk, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
