@@ -473,8 +473,11 @@ __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, 
     if (t < 4 || wave + 4 * t < 18) {
       dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
     } else {
-      const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
-      dma_b32(step_scales, 4 * (lane & 31), buf + 18432);
+      // byte offset of the lane's token scale, 4 (lane & 31), recomputed here
+      // (volatile: not hoisted) rather than held in a register across the loop
+      uint32_t voff;
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_and_b32 %0, 31, %0\n\tv_lshlrev_b32 %0, 2, %0" : "=v"(voff));
+      dma_b32(step_scales, voff, buf + 18432);
     }
   }
 }
@@ -1003,43 +1006,52 @@ void attend_kernel(AttendLaunch a) {
       }
     }
     __syncthreads();
-    float inv[4];
+    // Each head block goes through LDS (the ring is free: every wave is past
+    // its last PV and no load is in flight), so that the stores write whole
+    // rows (512 B of fp32 or 256 B of bf16 per head) instead of the
+    // accumulators' 32-byte pieces spread over 32 rows.  Each wave stages its
+    // own 128 columns; its LDS ops complete in order, so no barrier is needed.
+    // Accumulator lane: head 32hb + n32, columns 32cbl + 8q + 4h + [0, 4).
+    {
+      constexpr int kStageRow = 128 * 4 + 16;  // bytes per head, padded off the banks
+      static_assert(4 * 32 * kStageRow <= L::kRing, "epilogue staging fits in the ring");
+      // The addresses below are the same for every unit: laundering the lane
+      // coordinates here keeps the compiler from hoisting all of them out of
+      // the unit loop (and spilling them).
+      const int hl = (int)opaque((uint32_t)h), nl = (int)opaque((uint32_t)n32);
+      const uint8_t LDS_AS* wstage = sm + wave * 32 * kStageRow;
+      auto rows = [&](int hb, auto store) {
+        // rows 2k + h, 4 columns per lane: 32 lanes cover one head's 128;
+        // the row's normaliser (1 ulp reciprocal) is applied here
 #pragma unroll
-    for (int hb = 0; hb < 4; ++hb) inv[hb] = 1.f / l_lds[32 * hb + n32];
-    // lane: head 32hb + n32; 4 consecutive columns 32cb + 8rg + 4h + [0, 4)
-    if (slot < 0) {
-      uint8_t* orow = (uint8_t*)a.out + (size_t)tile * a.H * kDimV * 2;
-#pragma unroll
-      for (int hb = 0; hb < 4; ++hb) {
-        const int hh = 32 * hb + n32;
-        if (hh < a.H) {
-#pragma unroll
-          for (int cbl = 0; cbl < 4; ++cbl)
-#pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-              const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
-              u32x2 w;
-              w[0] = pack_bf16x2(o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb]);
-              w[1] = pack_bf16x2(o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]);
-              *(u32x2*)(orow + (size_t)hh * (kDimV * 2) + col * 2) = w;
-            }
+        for (int k = 0; k < 16; ++k) {
+          const int row = 2 * k + hl, hh = 32 * hb + row;
+          f32x4 v = *(const f32x4 LDS_AS*)(wstage + row * kStageRow + nl * 16);
+          v *= __builtin_amdgcn_rcpf(l_lds[hh]);
+          if (hh < a.H) store(hh, v);
         }
-      }
-    } else {
-      float* prow = a.ws.part_out + (size_t)slot * a.H * kDimV;
+      };
+      const size_t col = 128 * wave + 4 * nl;
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
-        const int hh = 32 * hb + n32;
-        if (hh < a.H) {
+        uint8_t LDS_AS* stage = sm + wave * 32 * kStageRow + nl * kStageRow + 16 * hl;
 #pragma unroll
-          for (int cbl = 0; cbl < 4; ++cbl)
+        for (int cbl = 0; cbl < 4; ++cbl)
 #pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-              const int col = 32 * (4 * wave + cbl) + 8 * rg + 4 * h;
-              const f32x4 w = {o[cbl][hb][4 * rg] * inv[hb], o[cbl][hb][4 * rg + 1] * inv[hb],
-                               o[cbl][hb][4 * rg + 2] * inv[hb], o[cbl][hb][4 * rg + 3] * inv[hb]};
-              *(f32x4*)(prow + (size_t)hh * kDimV + col) = w;
-            }
+          for (int q = 0; q < 4; ++q)
+            *(f32x4 LDS_AS*)(stage + (32 * cbl + 8 * q) * 4) =
+                (f32x4){o[cbl][hb][4 * q], o[cbl][hb][4 * q + 1], o[cbl][hb][4 * q + 2], o[cbl][hb][4 * q + 3]};
+        if (slot < 0) {
+          uint16_t* obase = (uint16_t*)a.out + (size_t)tile * a.H * kDimV + col;
+          rows(hb, [&](int hh, const f32x4& v) {
+            u32x2 w;
+            w[0] = pack_bf16x2(v[0], v[1]);
+            w[1] = pack_bf16x2(v[2], v[3]);
+            *(u32x2*)(obase + (size_t)hh * kDimV) = w;
+          });
+        } else {
+          float* pbase = a.ws.part_out + (size_t)slot * a.H * kDimV + col;
+          rows(hb, [&](int hh, const f32x4& v) { *(f32x4*)(pbase + (size_t)hh * kDimV) = v; });
         }
       }
     }
