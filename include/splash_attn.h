@@ -91,9 +91,12 @@ typedef struct splash_mla_desc {
  * SPLASH_DEFAULT_MAX_PARTIALS.  The planner never exceeds the capacity that
  * the passed ws_bytes provides: with too little room it splits less.
  * Layout (byte offsets from splash_mla_workspace_offsets, 256-byte aligned):
- *   [0] header int32[64]: [0] unit counter, [1] number of work units,
- *       [2] partial slots used, [3] pages per unit chosen, [4] debug status,
- *       [5] drained workers, [6] number of split tiles, [7] total pages
+ *   [0] header int32[1152]: [0] unit counter, [1] number of work units,
+ *       [2] partial slots used, [3] pages per unit chosen (0 for a fold
+ *       plan), [4] debug status, [5] drained workers, [6] number of split
+ *       tiles, [7] total pages, [8] most parts of a split tile, [9] workers of
+ *       a fold plan (0: queue), [10] the fold plan's cap; from [64] the fold
+ *       plan's first unit of each worker (workers + 1 entries)
  *   [1] work units int32[max_units][4] = {tile, first page, end page, slot},
  *       tile = b*q_chunk + i, slot = partial index or -1 (unit writes out/lse)
  *   [2] split offsets int32[B*q_chunk + 1] (partial slots of tile t are
@@ -191,14 +194,19 @@ int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table,
  * tests and for callers that want to inspect a plan.  It computes exactly
  * what splash_mla_plan computes on the device for `num_workers` compute units
  * and `max_partials` partial slots.  units_out: int32 [max_units][4];
- * indptr_out: int32 [B*q_chunk + 1]; stats_out: int32[4] = {units, partial
- * slots used, pages per unit, total pages}.  Returns SPLASH_OK, or
+ * indptr_out: int32 [B*q_chunk + 1]; stats_out: int32[7] = {units, partial
+ * slots used, pages per unit (0 for a fold plan), total pages, workers of a
+ * fold plan (0: the workers draw units from a queue), the pages a fold plan
+ * lets a long history keep (the rest goes to a second worker), the most
+ * parts of any split tile}; worker_start_out (may be NULL): int32
+ * [num_workers + 1], for a fold plan the first unit of each worker (worker g
+ * runs units [w[g], w[g+1])), untouched otherwise.  Returns SPLASH_OK, or
  * SPLASH_ERR_WORKSPACE_TOO_SMALL when max_units is too small.
  */
 int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk,
                          const splash_mla_desc* desc, int32_t num_workers,
                          int32_t max_partials, int32_t* units_out, int32_t max_units,
-                         int32_t* indptr_out, int32_t* stats_out);
+                         int32_t* indptr_out, int32_t* stats_out, int32_t* worker_start_out);
 
 /* Number of work units the workspace reserves: B*q_chunk + max_partials. */
 int32_t splash_mla_max_units(int32_t batch, int32_t q_chunk, int32_t max_partials);

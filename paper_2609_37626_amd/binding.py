@@ -71,7 +71,7 @@ _SIGNATURES = {
     "splash_mla_combine_splits": (ctypes.c_int, [_I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP]),
     "splash_mla_debug_gather": (ctypes.c_int, [_VP, _VP, _VP, _PD, _VP, _VP]),
-    "splash_mla_plan_host": (ctypes.c_int, [_PI32, _I32, _PD, _I32, _I32, _PI32, _I32, _PI32, _PI32]),
+    "splash_mla_plan_host": (ctypes.c_int, [_PI32, _I32, _PD, _I32, _I32, _PI32, _I32, _PI32, _PI32, _PI32]),
     "splash_mla_max_units": (_I32, [_I32, _I32, _I32]),
     "splash_device_workers": (_I32, []),
     "splash_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -202,20 +202,30 @@ def splash_mla_debug_gather(kv_pages, block_table, seq_lens, desc: MlaDesc, dens
 
 def splash_mla_plan_host(seq_lens: np.ndarray, q_chunk: int, desc: MlaDesc, num_workers: int,
                          max_partials: int = 0):
-    """Host mirror of the planner: returns (units [U,4], indptr [T+1], stats dict)."""
+    """Host mirror of the planner: returns (units [U,4], indptr [T+1], stats dict).
+
+    stats["fold"] tells a fold plan (each worker runs its own units) from a
+    plan of one unit size (workers draw units from a queue); for a fold plan
+    stats["cap"] is the pages a long tile keeps and stats["worker_start"]
+    the first unit of each of the num_workers workers and the end
+    (num_workers + 1 entries), else None.
+    """
     L = lib()
     seq = np.ascontiguousarray(seq_lens, dtype=np.int32)
     T = int(seq.shape[0]) * q_chunk
     max_units = int(L.splash_mla_max_units(int(seq.shape[0]), q_chunk, max_partials))
     units = np.zeros((max(max_units, 1), 4), dtype=np.int32)
     indptr = np.zeros(T + 1, dtype=np.int32)
-    stats = np.zeros(4, dtype=np.int32)
+    stats = np.zeros(7, dtype=np.int32)
+    wstart = np.zeros(num_workers + 1, dtype=np.int32)
     as_p = lambda a: a.ctypes.data_as(_PI32)
     _check(L.splash_mla_plan_host(as_p(seq), q_chunk, ctypes.byref(desc), num_workers, max_partials,
-                                  as_p(units), max_units, as_p(indptr), as_p(stats)))
+                                  as_p(units), max_units, as_p(indptr), as_p(stats), as_p(wstart)))
     n = int(stats[0])
+    fold = int(stats[4]) > 0
     return units[:n].copy(), indptr, {"units": n, "partials": int(stats[1]), "chunk_pages": int(stats[2]),
-                                      "total_pages": int(stats[3])}
+                                      "total_pages": int(stats[3]), "fold": fold, "cap": int(stats[5]),
+                                      "max_parts": int(stats[6]), "worker_start": wstart if fold else None}
 
 
 def version() -> str:

@@ -388,7 +388,7 @@ int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table, co
 
 int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const splash_mla_desc* desc,
                          int32_t num_workers, int32_t max_partials, int32_t* units_out, int32_t max_units,
-                         int32_t* indptr_out, int32_t* stats_out) {
+                         int32_t* indptr_out, int32_t* stats_out, int32_t* worker_start_out) {
   int st = validate_desc(desc, q_chunk);
   if (st != SPLASH_OK) return st;
   if (num_workers < 1) return fail(SPLASH_ERR_INVALID_ARGUMENT, "num_workers must be >= 1");
@@ -396,28 +396,28 @@ int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const sp
   if (B > 0 && (!seq_lens_host || !units_out || !indptr_out || !stats_out))
     return fail(SPLASH_ERR_INVALID_ARGUMENT, "NULL host buffer");
   if (max_partials <= 0) max_partials = SPLASH_DEFAULT_MAX_PARTIALS;
-  auto pages = [&](int32_t t) {
-    const int32_t b = t / q_chunk, i = t - b * q_chunk;
-    const int32_t L = tile_keys(seq_lens_host[b], q_chunk, i);
-    return L > 0 ? ceil_div(L, kPage) : 0;
-  };
+  const int32_t G = num_workers;
+  std::vector<int32_t> P((size_t)std::max(T, 1));
   int64_t total = 0;
   int32_t mx = 0;
   for (int32_t t = 0; t < T; ++t) {
-    total += pages(t);
-    mx = std::max(mx, pages(t));
+    const int32_t b = t / q_chunk, i = t - b * q_chunk;
+    const int32_t L = tile_keys(seq_lens_host[b], q_chunk, i);
+    P[t] = L > 0 ? ceil_div(L, kPage) : 0;
+    total += P[t];
+    mx = std::max(mx, P[t]);
   }
   const int32_t max_pages = mx > 0 ? mx : 1;
   const int32_t cap_units = std::min<int64_t>(max_units, (int64_t)T + max_partials);
   auto evaluate = [&](int32_t c, int64_t* cost) {
     int64_t W = 0, S = 0;
     for (int32_t t = 0; t < T; ++t) {
-      const int32_t P = pages(t), n = P > 0 ? ceil_div(P, c) : 0;
+      const int32_t n = P[t] > 0 ? ceil_div(P[t], c) : 0;
       W += n;
       S += n > 1 ? n : 0;
     }
     const bool ok = S <= max_partials && W <= (int64_t)T + max_partials;
-    *cost = ok ? plan_cost(c, W, S, total, max_pages, num_workers, kPlanCosts) : INT64_MAX;
+    *cost = ok ? plan_cost(c, W, S, total, max_pages, G, kPlanCosts) : INT64_MAX;
   };
   int32_t best_c = 0;
   int64_t best = INT64_MAX;
@@ -430,45 +430,101 @@ int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const sp
       best_c = c;
     }
   }
-  if (desc->flags & SPLASH_FLAG_FORCE_SPLIT) {
+  const bool forced = (desc->flags & SPLASH_FLAG_FORCE_SPLIT) != 0;
+  if (forced) {
     const int32_t c = std::min(desc->split_pages, (int32_t)kMaxUnitPages);
     int64_t cost;
     evaluate(c, &cost);
     if (cost != INT64_MAX) best_c = c;
   }
   const int32_t c = best_c;
-  int32_t nu = 0, ns = 0;
-  for (int32_t t = 0; t < T; ++t) {
-    const int32_t P = pages(t), n = P > 0 ? ceil_div(P, c) : 0;
-    indptr_out[t] = ns;
-    for (int32_t u = 0; u < n; ++u) {
-      if (nu >= cap_units) return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "more units than max_units");
-      int32_t* r = units_out + 4 * (size_t)nu++;
-      r[0] = t;
-      r[1] = unit_begin(P, n, u);
-      r[2] = unit_begin(P, n, u + 1);
-      r[3] = n > 1 ? ns + u : -1;
+  // the fold plan: ranks by pages (longest first, ties by tile), then the
+  // cheapest cap, largest on ties
+  bool fold = !forced && fold_applicable(T, G, kMaxWorkers, max_pages, total, best, kPlanCosts);
+  int32_t cap = 0, nl = 0;
+  std::vector<int32_t> q((size_t)std::max(G, 1), 0), rank_tile((size_t)std::max(T, 1));
+  if (fold) {
+    for (int32_t t = 0; t < T; ++t) rank_tile[t] = t;
+    std::stable_sort(rank_tile.begin(), rank_tile.begin() + T, [&](int32_t a, int32_t b) { return P[a] > P[b]; });
+    for (int32_t r = 0; r < T; ++r) q[r] = P[rank_tile[r]];
+    int64_t fbest = INT64_MAX;
+    for (int32_t C = q[0] - 1; C >= 1; --C) {
+      int32_t n;
+      const int64_t cost = fold_cost(C, q, G, max_partials, kPlanCosts, &n);
+      if (cost < fbest) {
+        fbest = cost;
+        cap = C;
+      }
     }
-    ns += n > 1 ? n : 0;
+    fold = fbest != INT64_MAX && fbest < best;
+    if (fold) fold_cost(cap, q, G, max_partials, kPlanCosts, &nl);
   }
-  if (T >= 0 && indptr_out) indptr_out[T] = ns;
-  if (T <= kPlanLdsTiles && nu > num_workers) {
-    // the device queue order: longest unit first (equal lengths in tile
-    // order here; the device leaves their order open)
-    std::vector<std::array<int32_t, 4>> rows((size_t)nu);
-    for (int32_t i = 0; i < nu; ++i)
-      for (int j = 0; j < 4; ++j) rows[i][j] = units_out[4 * (size_t)i + j];
-    std::stable_sort(rows.begin(), rows.end(), [](const std::array<int32_t, 4>& a, const std::array<int32_t, 4>& b) {
-      return a[2] - a[1] > b[2] - b[1];
-    });
-    for (int32_t i = 0; i < nu; ++i)
-      for (int j = 0; j < 4; ++j) units_out[4 * (size_t)i + j] = rows[i][j];
+  int32_t nu = 0, ns = 0;
+  if (fold) {
+    // partial slots in tile order; units worker by worker
+    for (int32_t t = 0; t < T; ++t) {
+      indptr_out[t] = ns;
+      ns += P[t] > cap ? 2 : 0;
+    }
+    indptr_out[T] = ns;
+    if ((int64_t)T + nl > cap_units) return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "more units than max_units");
+    for (int32_t r = 0; r < G; ++r) {
+      if (worker_start_out) worker_start_out[r] = nu;
+      if (r < T && q[r] > 0) {
+        const int32_t t = rank_tile[r];
+        int32_t* u = units_out + 4 * (size_t)nu++;
+        u[0] = t;
+        u[1] = 0;
+        u[2] = r < nl ? cap : q[r];
+        u[3] = r < nl ? indptr_out[t] : -1;
+      }
+      if (r >= G - nl) {
+        const int32_t j = G - 1 - r, t = rank_tile[j];
+        int32_t* u = units_out + 4 * (size_t)nu++;
+        u[0] = t;
+        u[1] = cap;
+        u[2] = q[j];
+        u[3] = indptr_out[t] + 1;
+      }
+    }
+    if (worker_start_out) worker_start_out[G] = nu;
+  } else {
+    for (int32_t t = 0; t < T; ++t) {
+      const int32_t n = P[t] > 0 ? ceil_div(P[t], c) : 0;
+      indptr_out[t] = ns;
+      for (int32_t u = 0; u < n; ++u) {
+        if (nu >= cap_units) return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "more units than max_units");
+        int32_t* r = units_out + 4 * (size_t)nu++;
+        r[0] = t;
+        r[1] = unit_begin(P[t], n, u);
+        r[2] = unit_begin(P[t], n, u + 1);
+        r[3] = n > 1 ? ns + u : -1;
+      }
+      ns += n > 1 ? n : 0;
+    }
+    if (T >= 0 && indptr_out) indptr_out[T] = ns;
+    if (T <= kPlanLdsTiles && nu > G) {
+      // the device queue order: longest unit first (equal lengths in tile
+      // order here; the device leaves their order open)
+      std::vector<std::array<int32_t, 4>> rows((size_t)nu);
+      for (int32_t i = 0; i < nu; ++i)
+        for (int j = 0; j < 4; ++j) rows[i][j] = units_out[4 * (size_t)i + j];
+      std::stable_sort(rows.begin(), rows.end(),
+                       [](const std::array<int32_t, 4>& a, const std::array<int32_t, 4>& b) {
+                         return a[2] - a[1] > b[2] - b[1];
+                       });
+      for (int32_t i = 0; i < nu; ++i)
+        for (int j = 0; j < 4; ++j) units_out[4 * (size_t)i + j] = rows[i][j];
+    }
   }
   if (stats_out) {
     stats_out[0] = nu;
     stats_out[1] = ns;
-    stats_out[2] = c;
+    stats_out[2] = fold ? 0 : c;
     stats_out[3] = total > INT32_MAX ? INT32_MAX : (int32_t)total;
+    stats_out[4] = fold ? G : 0;
+    stats_out[5] = fold ? cap : 0;
+    stats_out[6] = fold ? (nl > 0 ? 2 : 1) : (max_pages + c - 1) / c;
   }
   return SPLASH_OK;
 }

@@ -2,8 +2,9 @@
 // combine, page gather and device-data check.
 //
 // Attend kernel design (one persistent workgroup per compute unit):
-//  * Work unit = (query row n with all H heads, page range).  Units come from
-//    a device queue filled by the planner; workers draw them with one atomic.
+//  * Work unit = (query row n with all H heads, page range).  Under a fold
+//    plan each worker runs its own run of units; otherwise units come from a
+//    device queue filled by the planner, drawn with one atomic.
 //  * 4 waves; wave w owns heads [32w, 32w+32).  Its 32 query rows stay in
 //    VGPRs for the whole unit (36 x 16-byte MFMA B fragments).
 //  * KV is staged 32 rows (half a page, one "step") at a time straight from
@@ -128,6 +129,18 @@ __device__ __forceinline__ int32_t wave_incl_scan(int32_t x) {
   return x;
 }
 
+// Inclusive running max of one non-negative int per lane over the wave (the
+// same DPP pattern as the scan, with max for the add).
+__device__ __forceinline__ int32_t wave_incl_max(int32_t x) {
+  x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+  x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+  x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+  x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+  x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false));  // row_bcast:15 -> rows 1, 3
+  x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false));  // row_bcast:31 -> rows 2, 3
+  return x;
+}
+
 // Exclusive block scan of one int per thread (1024 threads); returns the
 // exclusive prefix and writes the block total to *total.
 __device__ int32_t block_exclusive_scan(int32_t v, int32_t* wave_buf, int32_t* total) {
@@ -153,19 +166,23 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ int32_t s_pages[kPlanLdsTiles];
   __shared__ int32_t s_ufirst[kPlanLdsTiles + 1];  // first unit of each tile (cached case)
   __shared__ int32_t s_sfirst[kPlanLdsTiles];      // first partial slot of each tile (cached case)
+  __shared__ int64_t s_w[16][kNumCandidates + 1], s_s[16][kNumCandidates + 1];  // units, split units per tile slice
+  __shared__ int32_t s_lhist[kMaxUnitPages + 1];  // units per length
+  __shared__ int32_t s_lbase[kMaxUnitPages + 1];  // next queue slot per length
+  __shared__ int32_t s_q[kMaxWorkers];            // fold plan: pages of each rank (0 past the last tile)
+  __shared__ int32_t s_rt[kMaxWorkers];           // fold plan: tile of each rank
+  __shared__ int32_t s_pm[kMaxWorkers / 2];       // fold plan: running max of the pair loads
   __shared__ int64_t s_red64[16];
   __shared__ int32_t s_red32[16];
   __shared__ int64_t s_cost[kNumCandidates + 1];
-  __shared__ int64_t s_w[16][kNumCandidates + 1], s_s[16][kNumCandidates + 1];  // units, split units per tile slice
   __shared__ int32_t s_list[kNumCandidates + 1];  // candidate index of each distinct size
   __shared__ int32_t s_nd;                        // number of distinct sizes
   __shared__ UDiv s_udiv[kNumCandidates + 1];      // their division magic
   __shared__ int32_t s_cand[kNumCandidates + 1];
   __shared__ int32_t s_parts[kNumCandidates];  // parts of each candidate
-  __shared__ int32_t s_lhist[kMaxUnitPages + 1];  // units per length
-  __shared__ int32_t s_lbase[kMaxUnitPages + 1];  // next queue slot per length
   __shared__ int32_t s_scan[17];
   __shared__ int32_t s_chunk;
+  __shared__ int64_t s_best;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t T = p.B * p.q_chunk;
   const bool cached = T <= kPlanLdsTiles;
@@ -290,6 +307,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     int bk = best == INT64_MAX ? kNumCandidates : (int)(best & 127);
     if (lane == 0) {
       if (bk >= kNumCandidates) bk = 0;
+      s_best = best == INT64_MAX ? INT64_MAX : (best >> 7);
       if (p.forced_chunk > 0 && s_cost[kNumCandidates] != INT64_MAX) bk = kNumCandidates;
       s_chunk = s_cand[bk];
     }
@@ -297,14 +315,97 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __syncthreads();
   const int32_t c = s_chunk;
 
+  // 2b. the fold plan (at most one tile per worker, no forced size): rank
+  // the tiles by pages, then price every cap (thread C - 1 takes cap C) and
+  // keep the cheapest; taken when it beats every unit size.  The busiest worker under cap C is
+  // max(16 C + U, max_{j < nl(C)} v_j - 16 C) with v_j = 16 (q_j + q_{G-1-j})
+  // + U + U [q_{G-1-j} > 0] independent of C, so a running max of v over j
+  // and a binary search for nl(C) = #{r : q_r > C} price a cap in O(log G).
+  bool fold = p.forced_chunk == 0 &&
+              fold_applicable(T, p.G, kMaxWorkers, max_pages, total_pages, s_best, kPlanCosts);  // uniform
+  int32_t cap = 0, nl = 0;
+  if (fold) {
+    // counting sort of the tiles by pages, longest first: the histogram, the
+    // number of tiles with more pages (thread i takes pages kMaxUnitPages -
+    // i), then one atomic per tile (tiles of equal pages in whatever order
+    // the atomics give; it decides only which worker runs which of them)
+    for (int32_t i = tid; i <= kMaxUnitPages; i += 1024) s_lhist[i] = 0;
+    __syncthreads();
+    if (tid < T) atomicAdd(&s_lhist[s_pages[tid]], 1);  // 0 <= pages <= kMaxUnitPages
+    __syncthreads();
+    int32_t longer;
+    s_lbase[kMaxUnitPages - tid] = block_exclusive_scan(s_lhist[kMaxUnitPages - tid], s_scan, &longer);
+    if (tid == 0) s_lbase[0] = longer;  // empty tiles last
+    __syncthreads();
+    if (tid < T) {
+      const int32_t P = s_pages[tid], r = atomicAdd(&s_lbase[P], 1);
+      s_q[r] = P;
+      s_rt[r] = tid;
+    } else if (tid < p.G) {
+      s_q[tid] = 0;
+    }
+    __syncthreads();
+    const int32_t U = kPlanCosts.unit_x16, half = p.G / 2;
+    int32_t v = 0;
+    if (tid < half) {
+      const int32_t qk = s_q[p.G - 1 - tid];
+      v = 16 * (s_q[tid] + qk) + U + (qk > 0 ? U : 0);
+    }
+    v = wave_incl_max(v);  // running max inside the wave, then over the waves before
+    if (lane == 63) s_red32[wave] = v;
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) v = s_red32[w] > v ? s_red32[w] : v;
+    if (tid < half) s_pm[tid] = v;
+    __syncthreads();
+    auto count_long = [&](int32_t C) {  // first rank with q_r <= C (q descends)
+      int32_t lo = 0, hi = T;
+      while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (s_q[mid] > C) lo = mid + 1; else hi = mid;
+      }
+      return lo;
+    };
+    const int32_t C = tid + 1;
+    int64_t key = INT64_MAX;
+    if (C < s_q[0]) {
+      const int32_t n = count_long(C);
+      if (2 * n <= p.G && 2 * n <= p.ws.max_partials) {
+        int64_t mk = 16 * (int64_t)C + U;
+        if (n > 0 && (int64_t)s_pm[n - 1] - 16 * C > mk) mk = (int64_t)s_pm[n - 1] - 16 * C;
+        const int64_t cost = (int64_t)p.G * (mk + kPlanCosts.split_x16) + 2 * (int64_t)n * kPlanCosts.combine_x16;
+        key = (cost << 10) | (kMaxUnitPages - C);  // ties: the larger cap
+      }
+    }
+    key = __ockl_wfred_min_i64(key);
+    __syncthreads();  // every wave is past its reads of s_red32
+    if (lane == 0) s_red64[wave] = key;
+    __syncthreads();
+    key = INT64_MAX;
+    for (int w = 0; w < 16; ++w) key = s_red64[w] < key ? s_red64[w] : key;
+    fold = key != INT64_MAX && (key >> 10) < s_best;
+    if (fold) {
+      cap = kMaxUnitPages - (int32_t)(key & 1023);
+      nl = count_long(cap);
+    }
+  }
+  auto tile_units = [&](int32_t t, int32_t P, int32_t* n, int32_t* sp) {
+    if (fold) {
+      *n = P > cap ? 2 : (P > 0 ? 1 : 0);
+      *sp = P > cap ? 2 : 0;
+    } else {
+      *n = P > 0 ? ceil_div(P, c) : 0;
+      *sp = *n > 1 ? *n : 0;
+    }
+  };
+
   // 3. scan units / partial slots / split tiles over the tiles, write the list.
   int32_t carry_u = 0, carry_s = 0, carry_f = 0;
   for (int32_t base = 0; base < T; base += 1024) {
     const int32_t t = base + tid;
     const int32_t P = t < T ? pages_of(t) : 0;
-    const int32_t n = P > 0 ? ceil_div(P, c) : 0;
-    const int32_t sp = n > 1 ? n : 0;
-    const int32_t f = n > 1 ? 1 : 0;
+    int32_t n = 0, sp = 0;
+    if (t < T) tile_units(t, P, &n, &sp);
+    const int32_t f = sp > 0 ? 1 : 0;
     int32_t tu, ts, tf;
     const int32_t eu = block_exclusive_scan(n, s_scan, &tu) + carry_u;
     const int32_t es = block_exclusive_scan(sp, s_scan, &ts) + carry_s;
@@ -335,18 +436,37 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     carry_s += ts;
     carry_f += tf;
   }
-  // 4. unit records, one thread per unit (cached case): find the tile by
-  // binary search over the first-unit offsets.  With more units than workers
-  // the queue is ordered longest unit first (a counting sort over unit
-  // lengths; the order among units of equal length is whatever the LDS
-  // atomics give, and does not change any result), so the persistent workers
-  // pack the units the way a longest-processing-time-first schedule would.
-  // With at most one unit per worker every unit starts at once: tile order.
-  if (cached) {
+  // 4. unit records.  A fold plan writes them worker by worker (worker r:
+  // its own tile, or the head of it, then the tail it takes over) together
+  // with each worker's first unit.  Otherwise (cached case) one thread per
+  // unit finds its tile by binary search over the first-unit offsets; with
+  // more units than workers the queue is ordered longest unit first (a
+  // counting sort over unit lengths; the order among units of equal length
+  // is whatever the LDS atomics give, and does not change any result), so the
+  // persistent workers pack the units the way a longest-processing-time-first
+  // schedule would; with at most one unit per worker every unit starts at
+  // once: tile order.
+  if (fold) {
+    __syncthreads();  // partial offsets of every tile
+    const int32_t r = tid;
+    const bool own = r < T && s_q[r] > 0, tail = r < p.G && r >= p.G - nl;
+    int32_t total;
+    const int32_t base = block_exclusive_scan((int32_t)own + (int32_t)tail, s_scan, &total);
+    if (own) {
+      const int32_t t = s_rt[r], P = s_q[r];
+      p.ws.units[base] = r < nl ? make_int4(t, 0, cap, s_sfirst[t]) : make_int4(t, 0, P, -1);
+    }
+    if (tail) {
+      const int32_t j = p.G - 1 - r, t = s_rt[j];
+      p.ws.units[base + (int32_t)own] = make_int4(t, cap, s_q[j], s_sfirst[t] + 1);
+    }
+    if (r < p.G) hdr[kHdrWorkerTable + r] = base;
+    if (r == 0) hdr[kHdrWorkerTable + p.G] = total;
+  } else if (cached) {
     if (tid == 0) s_ufirst[T] = carry_u;
     for (int32_t i = tid; i <= kMaxUnitPages; i += 1024) s_lhist[i] = 0;
     __syncthreads();
-    const int32_t U = carry_u < p.ws.max_units ? carry_u : p.ws.max_units;
+    const int32_t NU = carry_u < p.ws.max_units ? carry_u : p.ws.max_units;
     auto unit_rec = [&](int32_t ug) {
       int32_t lo = 0, hi = T - 1;  // last tile with s_ufirst[t] <= ug
       while (lo < hi) {
@@ -364,8 +484,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       rec.w = n > 1 ? es + u : -1;
       return rec;
     };
-    const bool lpt = U > p.G;  // uniform
-    for (int32_t ug = tid; ug < U; ug += 1024) {
+    const bool lpt = NU > p.G;  // uniform
+    for (int32_t ug = tid; ug < NU; ug += 1024) {
       const int4 rec = unit_rec(ug);
       if (lpt) atomicAdd(&s_lhist[rec.z - rec.y], 1);  // 1 <= length <= kMaxUnitPages
       else p.ws.units[ug] = rec;
@@ -379,7 +499,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       int32_t unused;
       s_lbase[len] = block_exclusive_scan(s_lhist[len], s_scan, &unused);
       __syncthreads();
-      for (int32_t ug = tid; ug < U; ug += 1024) {
+      for (int32_t ug = tid; ug < NU; ug += 1024) {
         const int4 rec = unit_rec(ug);
         p.ws.units[atomicAdd(&s_lbase[rec.z - rec.y], 1)] = rec;
       }
@@ -391,10 +511,13 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     hdr[kHdrDone] = 0;
     hdr[kHdrUnits] = carry_u < p.ws.max_units ? carry_u : p.ws.max_units;
     hdr[kHdrPartials] = carry_s;
-    hdr[kHdrChunk] = c;
+    hdr[kHdrChunk] = fold ? 0 : c;
     hdr[kHdrSplitTiles] = carry_f;
     hdr[kHdrTotalPages] = total_pages > INT32_MAX ? INT32_MAX : (int32_t)total_pages;
-    hdr[kHdrMaxParts] = (max_pages + c - 1) / c;  // every tile has ceil(P / c) <= this many
+    // every split tile has at most this many parts
+    hdr[kHdrMaxParts] = fold ? (nl > 0 ? 2 : 1) : (max_pages + c - 1) / c;
+    hdr[kHdrSchedule] = fold ? p.G : 0;
+    hdr[kHdrFoldCap] = fold ? cap : 0;
   }
 }
 
@@ -662,10 +785,16 @@ void attend_kernel(AttendLaunch a) {
     }
   }
 
-  for (;;) {
+  // A fold plan made for this many workers gives each its own run of units;
+  // otherwise (or if the plan was made for another worker count) the workers
+  // draw units from the queue.
+  const bool own_run = a.ws.header[kHdrSchedule] == (int32_t)gridDim.x;
+  int32_t next = own_run ? a.ws.header[kHdrWorkerTable + blockIdx.x] : 0;
+  const int32_t last = own_run ? a.ws.header[kHdrWorkerTable + blockIdx.x + 1] : num_units;
+  for (;; ++next) {
     if (tid == 0) {
-      int32_t u = atomicAdd(&a.ws.header[kHdrGrab], 1);
-      s_unit = u < num_units ? a.ws.units[u] : make_int4(-1, 0, 0, 0);
+      const int32_t u = own_run ? next : atomicAdd(&a.ws.header[kHdrGrab], 1);
+      s_unit = u < last ? a.ws.units[u] : make_int4(-1, 0, 0, 0);
     }
     __syncthreads();
     const int4 unit = s_unit;

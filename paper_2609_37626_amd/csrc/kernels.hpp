@@ -30,6 +30,10 @@ enum HeaderSlot : int {
   kHdrSplitTiles = 6,  // number of tiles with partials
   kHdrTotalPages = 7,
   kHdrMaxParts = 8,    // upper bound on the parts of any split tile
+  kHdrSchedule = 9,    // 0: workers draw units from the queue; G > 0: fold plan for G workers,
+                       // worker g runs units [table[g], table[g + 1])
+  kHdrFoldCap = 10,    // fold plan: pages a long tile keeps (its tail goes to a partner worker)
+  kHdrWorkerTable = 64,  // fold plan: first unit of each worker, G + 1 entries
 };
 
 struct PlanLaunch {

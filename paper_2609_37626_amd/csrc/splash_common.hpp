@@ -20,7 +20,8 @@ constexpr int kDimV = 512;         // d_z = d_c
 constexpr int kMaxHeads = 128;
 constexpr int kStepKeys = 32;      // keys per pipeline step (half a page)
 constexpr int kMaxUnitPages = 1024;  // the block-table slice of one unit is staged in LDS
-constexpr int kHeaderInts = 64;
+constexpr int kMaxWorkers = 1024;    // the fold plan's per-worker table is sized for this many
+constexpr int kHeaderInts = 1152;    // 64 header slots, then the per-worker table (kMaxWorkers + 1)
 constexpr int kPlanLdsTiles = 8192;  // planner: tile data cached in LDS, and the unit queue ordered longest
                                      // first, up to this many tiles
 
@@ -39,12 +40,13 @@ constexpr int kPlanLdsTiles = 8192;  // planner: tile data cached in LDS, and th
 // page equivalents, scaled by 16 G so the arithmetic is integral.
 
 struct PlanCosts {
-  int32_t unit_x16;     // per unit on the busiest worker, pages * 16
+  int32_t unit_x16;     // per unit on the busiest worker (query load, pipeline fill and drain,
+                        // output store: about six pages of steps), pages * 16
   int32_t split_x16;    // per split unit on the busiest worker (partial write), pages * 16
   int32_t combine_x16;  // per partial, spread over the workers (combine read), pages * 16
 };
 
-constexpr PlanCosts kPlanCosts = {16, 32, 48};
+constexpr PlanCosts kPlanCosts = {96, 32, 48};
 constexpr int kNumCandidates = 96;
 
 SPLASH_HD int32_t tile_keys(int32_t seq_len, int32_t q_chunk, int32_t i) {
@@ -126,6 +128,57 @@ SPLASH_HD int64_t plan_cost(int32_t c, int64_t W, int64_t S, int64_t total_pages
 SPLASH_HD int32_t unit_begin(int32_t P, int32_t n, int32_t u) {
   if (P < 46341) return (int32_t)(((uint32_t)P * (uint32_t)u) / (uint32_t)n);  // product fits in 31 bits
   return (int32_t)(((int64_t)P * u) / n);
+}
+
+// ----------------------------------------------------------- fold plan --
+//
+// For at most one tile per worker (T <= G) the second kind of plan keeps
+// tiles whole except the longest.  Ranks r = 0 .. G-1 order the tiles by
+// pages, longest first (the host mirror breaks ties by tile index, the
+// device in whatever order its atomics give: a tie decides only which worker
+// runs which of two equal units), with q_r = 0 for the ranks
+// T .. G-1 that have no tile; worker r runs rank r's tile.  For a cap C every
+// tile with q_j > C ("long", ranks j < nl) keeps its first C pages and hands
+// the rest, its tail, to worker G-1-j: an idle worker, or the one with the
+// j-th shortest tile.  That needs 2 nl <= G.  In pages * 16, with U the fixed
+// cost of a unit, the busiest worker then runs
+//     max(16 C + U,  max_{j < nl} 16 (q_{G-1-j} + q_j - C) + U + U [q_{G-1-j} > 0])
+// and every long tile leaves two partials for the combine.  C is chosen over
+// 1 .. q_0 - 1 by the same estimate as the unit size (ties to the larger C),
+// and the fold plan is taken when it beats every unit size.  Every piece is
+// at most max_pages, so the fold needs max_pages <= kMaxUnitPages.
+
+// Estimated step time of cap C given pages by rank q[0..G), or INT64_MAX if
+// infeasible (a partner would be long, or the partials exceed max_partials);
+// *nl_out = long tiles.
+template <typename Q>
+SPLASH_HD int64_t fold_cost(int32_t C, const Q& q, int32_t G, int32_t max_partials, PlanCosts k,
+                            int32_t* nl_out) {
+  int64_t mk = 16 * (int64_t)C + k.unit_x16;
+  int32_t nl = 0;
+  while (nl < G && q[nl] > C) {
+    const int32_t j = nl++;
+    if (2 * nl > G || 2 * nl > max_partials) return INT64_MAX;
+    const int32_t qk = q[G - 1 - j];
+    const int64_t pair = 16 * (int64_t)(qk + q[j] - C) + k.unit_x16 + (qk > 0 ? k.unit_x16 : 0);
+    mk = pair > mk ? pair : mk;
+  }
+  *nl_out = nl;
+  return (int64_t)G * (mk + k.split_x16) + 2 * (int64_t)nl * k.combine_x16;
+}
+
+// The fold plan is considered for T <= G <= max_workers tiles of at most
+// kMaxUnitPages pages, at least one of them longer than a page, and only
+// when it could beat the best unit size: every cap cuts the longest tile in
+// two, so the busiest worker runs at least half of it (and at least the
+// mean), a lower bound on every fold's estimate.
+SPLASH_HD bool fold_applicable(int32_t T, int32_t G, int32_t max_workers, int32_t max_pages, int64_t total_pages,
+                               int64_t best_cost, PlanCosts k) {
+  if (!(T >= 1 && T <= G && G <= max_workers && max_pages >= 2 && max_pages <= kMaxUnitPages)) return false;
+  int64_t busy = 8 * (int64_t)max_pages + k.unit_x16;
+  const int64_t mean = 16 * total_pages / G;
+  if (mean > busy) busy = mean;
+  return (int64_t)G * (busy + k.split_x16) < best_cost;
 }
 
 // ------------------------------------------------------------- LDS layout --

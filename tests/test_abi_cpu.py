@@ -161,6 +161,8 @@ def test_host_plan_covers_every_page_once(cfg):
         d.kv_scales = FAKE
     units, indptr, stats = B.splash_mla_plan_host(seq, spec.q_chunk, d, 256, 0)
     check_plan(seq, spec.q_chunk, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+    if stats["fold"]:
+        check_fold(seq, spec.q_chunk, units, stats, 256)
     again = B.splash_mla_plan_host(seq, spec.q_chunk, d, 256, 0)
     assert np.array_equal(units, again[0]) and np.array_equal(indptr, again[1])
 
@@ -174,12 +176,89 @@ def test_host_plan_splits_few_long_and_balances():
     assert sizes.max() <= 1.3 * stats["total_pages"] / 256 + 1
 
 
-def test_host_plan_keeps_many_short_requests_whole():
-    # one short history per worker: splitting would only add partial traffic
+UNIT_X16 = 96   # the planner's fixed cost of a unit, pages * 16
+
+
+def worker_loads(units, stats):
+    ws = stats["worker_start"]
+    w = 16 * (units[:, 2] - units[:, 1]).astype(np.int64) + UNIT_X16
+    return np.array([w[ws[g]:ws[g + 1]].sum() for g in range(len(ws) - 1)])
+
+
+def fold_makespan(pages, cap, G):
+    """The busiest worker of a fold with this cap, from its definition: ranks
+    by pages (longest first), the j-th longest tile above the cap hands its
+    tail to worker G-1-j."""
+    q = sorted(pages, reverse=True) + [0] * (G - len(pages))
+    loads = [16 * x + UNIT_X16 if x > 0 else 0 for x in q]
+    for j in range(G):
+        if q[j] <= cap:
+            break
+        loads[j] = 16 * cap + UNIT_X16
+        loads[G - 1 - j] += 16 * (q[j] - cap) + UNIT_X16
+    return max(loads)
+
+
+def check_fold(seq_lens, q_chunk, units, stats, G):
+    ws = stats["worker_start"]
+    assert stats["fold"] and stats["chunk_pages"] == 0 and len(ws) == G + 1
+    assert ws[0] == 0 and ws[-1] == stats["units"] and np.all(np.diff(ws) >= 0)
+    # a worker runs at most its own tile and one tail; split tiles have two
+    # parts: the head [0, cap) and the tail [cap, P)
+    assert np.diff(ws).max() <= 2 and stats["max_parts"] <= 2
+    split = units[units[:, 3] >= 0]
+    assert np.all((split[:, 1] == 0) & (split[:, 2] == stats["cap"]) | (split[:, 1] == stats["cap"]))
+    pages = [-(-(int(seq_lens[t // q_chunk]) - q_chunk + t % q_chunk + 1) // 64) for t in range(len(seq_lens) * q_chunk)]
+    loads = worker_loads(units, stats)
+    assert loads.max() == fold_makespan(pages, stats["cap"], G)
+    return loads
+
+
+def test_host_plan_folds_many_short_requests():
+    # one short history per worker, 16-64 pages: one unit each would leave
+    # the busiest worker with 64 pages while the mean is 41, so the longest
+    # histories keep a head of `cap` pages and hand their tails to the
+    # workers with the shortest ones
     seq, spec = _lengths(2)
     d = B.make_desc(256, 128, 64, int((-(-seq // 64)).sum()))
     units, indptr, stats = B.splash_mla_plan_host(seq, 1, d, 256, 0)
-    assert stats["units"] == 256 and stats["partials"] == 0
+    check_plan(seq, 1, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+    loads = check_fold(seq, 1, units, stats, 256)
+    assert loads.max() < 0.8 * (16 * 64 + UNIT_X16)
+    assert stats["partials"] < 256
+
+
+def test_host_plan_equal_tiles_stay_whole():
+    # equal histories, one per worker: nothing to balance, no partials
+    seq = np.full(256, 640, np.int32)
+    d = B.make_desc(256, 128, 10, 2560)
+    units, indptr, stats = B.splash_mla_plan_host(seq, 1, d, 256, 0)
+    check_plan(seq, 1, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+    assert stats["partials"] == 0 and stats["units"] == 256
+
+
+def test_host_plan_fold_random_shapes():
+    # Random batches of at most one tile per worker: whenever the fold plan is
+    # taken it covers every page once, keeps runs of at most two units, and
+    # its busiest worker is the definition's makespan, no worse than one unit
+    # per tile.
+    rng = np.random.default_rng(7)
+    seen = 0
+    for trial in range(300):
+        G = int(rng.integers(2, 300))
+        qc = int(rng.choice([1, 1, 2, 4]))
+        Bn = max(1, int(rng.integers(1, G + 1)) // qc)
+        seq = rng.integers(qc, 64 * 200, size=Bn).astype(np.int32)
+        d = B.make_desc(Bn, 128, int(-(-seq.max() // 64)), int((-(-seq // 64)).sum()) + 1)
+        units, indptr, stats = B.splash_mla_plan_host(seq, qc, d, G, 0)
+        check_plan(seq, qc, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+        if not stats["fold"]:
+            continue
+        seen += 1
+        loads = check_fold(seq, qc, units, stats, G)
+        pages = [-(-(int(seq[t // qc]) - qc + t % qc + 1) // 64) for t in range(Bn * qc)]
+        assert loads.max() <= 16 * max(pages) + UNIT_X16
+    assert seen > 50
 
 
 def test_host_plan_respects_partial_capacity_and_forced_split():
@@ -199,20 +278,28 @@ def test_host_plan_single_short_request_is_one_unit():
     assert units.tolist() == [[0, 0, 1, -1]] and indptr.tolist() == [0, 0]
 
 
-@pytest.mark.parametrize("cfg", [4, 5])
-def test_host_plan_queue_order(cfg):
-    # the persistent workers take units in queue order.  With more units than
-    # workers the longest go first (ties in tile order), which packs them like
-    # a longest-processing-time-first schedule; with at most one unit per
-    # worker every unit starts at once and the queue stays in tile order.
+@pytest.mark.parametrize("cfg,split", [(2, 0), (4, 0), (5, 0), (4, 20), (5, 64), (2, 64)])
+def test_host_plan_queue_order(cfg, split):
+    # A fold plan lists units worker by worker (each worker runs its own).  A
+    # plan of one unit size puts its units in a queue the persistent workers
+    # draw from: with more units than workers the longest go first (ties in
+    # tile order), which packs them like a longest-processing-time-first
+    # schedule; with at most one unit per worker every unit starts at once
+    # and the queue stays in tile order.  A forced unit size always makes the
+    # second kind.
     seq, spec = _lengths(cfg)
     d = B.make_desc(spec.B, spec.H, int(-(-seq.max() // 64)), int((-(-seq // 64)).sum()), spec.kv_dtype)
     if spec.kv_dtype:
         d.kv_scales = FAKE
+    if split:
+        d.flags, d.split_pages = B.FLAG_FORCE_SPLIT, split
     units, indptr, stats = B.splash_mla_plan_host(seq, spec.q_chunk, d, 256, 0)
     key = units[:, 0].astype(np.int64) * (1 << 32) + units[:, 1]
     ln = units[:, 2] - units[:, 1]
-    if stats["units"] > 256:
+    assert stats["fold"] == (cfg == 2 and split == 0)
+    if stats["fold"]:
+        check_fold(seq, spec.q_chunk, units, stats, 256)
+    elif stats["units"] > 256:
         assert np.all(ln[:-1] >= ln[1:])
         same = ln[:-1] == ln[1:]
         assert np.all(key[:-1][same] < key[1:][same])

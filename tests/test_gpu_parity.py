@@ -73,6 +73,14 @@ CASES = {
     "heads48_q2": lambda: W.make_custom([70, 300, 2], H=48, q_chunk=2, seed=15),
     "heads16_single_tokens": lambda: W.make_custom([1, 1, 1], H=16, seed=16),
     "heads112_fp8_q1": lambda: W.make_custom([33, 640, 1999], H=112, kv_dtype=W.KV_FP8_E4M3, seed=17),
+    # batches whose plan is a fold (each worker runs its own units; the
+    # longest histories hand their tails to the workers with the shortest
+    # or to idle ones; ragged last pages)
+    "fold_many_short_B250": lambda: W.make_custom(
+        np.random.Generator(np.random.PCG64(31)).integers(64, 900, size=250, endpoint=True), H=128, seed=31),
+    "fold_chunk8_fp8_B20": lambda: W.make_custom(
+        np.random.Generator(np.random.PCG64(32)).integers(300, 1500, size=20, endpoint=True), H=128, q_chunk=8,
+        kv_dtype=W.KV_FP8_E4M3, seed=32),
 }
 
 
@@ -80,6 +88,10 @@ CASES = {
 def test_parity_against_oracle(name):
     batch = CASES[name]()
     print(f"case {name}: B={batch.B} H={batch.H} q={batch.q_chunk} lens={batch.seq_lens.tolist()[:12]}", flush=True)
+    if name.startswith("fold_"):
+        seq = np.asarray(batch.seq_lens, np.int32)
+        d = B.make_desc(batch.B, batch.H, int(-(-seq.max() // 64)), 1 << 20)
+        assert B.splash_mla_plan_host(seq, batch.q_chunk, d, B.device_workers(), 0)[2]["fold"]
     out, lse = gpu_attend(batch)
     assert_parity(batch, out, lse, label=name)
 
@@ -218,11 +230,26 @@ def test_device_plan_matches_host_plan(case):
     units, indptr, stats = B.splash_mla_plan_host(seq, q_chunk, d, B.device_workers(), 0)
     offs, _ = B.workspace_offsets(Bn, q_chunk, H, 0)
     raw = ws.cpu().numpy()
-    hdr = raw[offs[0]:offs[0] + 256].view(np.int32)
-    print(f"plan {case}: chunk {stats['chunk_pages']} units {stats['units']} partials {stats['partials']}", flush=True)
+    G = B.device_workers()
+    hdr = raw[offs[0]:offs[0] + 4 * (64 + G + 1)].view(np.int32)
+    print(f"plan {case}: chunk {stats['chunk_pages']} units {stats['units']} partials {stats['partials']} "
+          f"fold {stats['fold']}", flush=True)
     assert hdr[1] == stats["units"] and hdr[2] == stats["partials"] and hdr[3] == stats["chunk_pages"]
+    assert hdr[8] == stats["max_parts"] and hdr[9] == (G if stats["fold"] else 0)
     dev_units = raw[offs[1]:offs[1] + 16 * stats["units"]].view(np.int32).reshape(-1, 4)
-    if stats["units"] > B.device_workers():
+    if stats["fold"]:
+        # the same cap, units and worker runs; histories of equal length may
+        # sit at each other's ranks (the device orders ties with atomics), so
+        # each worker's run is compared by its unit lengths and the split
+        # pieces by their pages
+        assert hdr[10] == stats["cap"]
+        canon = lambda u: u[np.lexsort(u.T[::-1])]
+        assert np.array_equal(canon(dev_units), canon(units))
+        ws = stats["worker_start"]
+        assert np.array_equal(hdr[64:64 + G + 1], ws)
+        runs = lambda u: [sorted((u[a:b, 2] - u[a:b, 1]).tolist()) for a, b in zip(ws[:-1], ws[1:])]
+        assert runs(dev_units) == runs(units)
+    elif stats["units"] > G:
         # the same units (the device leaves the order of equal-length units
         # open), and both queues hand out the longest units first
         canon = lambda u: u[np.lexsort(u.T[::-1])]
