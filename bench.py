@@ -197,7 +197,7 @@ def main():
                 "attend_us_median": round(float(np.median([e[1].elapsed_time(e[2]) for e in cev])) * 1e3, 2)}
 
     offs, _ = B.workspace_offsets(batch.B, batch.q_chunk, batch.H, 0)
-    hdr = ws[offs[0]:offs[0] + 32].cpu().numpy().view(np.int32)
+    hdr = ws[offs[0]:offs[0] + 64].cpu().numpy().view(np.int32)
 
     kv_bytes, alg_bytes, flops = W.workload_bytes_flops(batch)
     attend_avg_s = float(attend_ms.mean()) * 1e-3
@@ -247,8 +247,9 @@ def main():
         "phases_us": {"plan": round(float(plan_ms.mean()) * 1e3, 2),
                       "attend": round(float(attend_ms.mean()) * 1e3, 2),
                       "combine": round(float(combine_ms.mean()) * 1e3, 2)},
-        "plan": {"units": int(hdr[1]), "partials": int(hdr[2]), "pages_per_unit": int(hdr[3]),
-                 "split_tiles": int(hdr[6]), "workers": B.device_workers()},
+        "plan": {"kind": "fold" if int(hdr[9]) > 0 else "unit size",
+                 "units": int(hdr[1]), "partials": int(hdr[2]), "pages_per_unit": int(hdr[3]),
+                 "fold_cap_pages": int(hdr[10]), "split_tiles": int(hdr[6]), "workers": B.device_workers()},
         "roofline": roof,
     }
     if cold is not None:
