@@ -88,6 +88,100 @@ def cpu_baseline(batch, budget_s):
             "cpu_threads_available": len(os.sched_getaffinity(0))}
 
 
+def run_sharded(args, spec, batch, db):
+    """--shards N: every history cut into N page-aligned position shards of
+    (nearly) equal length; a step is the N shard calls (each: plan, attend,
+    the shard's own combine) and one splash_mla_combine over the N partials,
+    i.e. what N position-sharded ranks compute, on one GPU."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37626_amd import binding as B
+    from paper_2609_37626_amd import workloads as W
+
+    N = args.shards
+    s = batch.seq_lens.astype(np.int64)
+    cuts = np.stack([np.minimum(s, (s * k // N) // 64 * 64) for k in range(N)] + [s], axis=1).astype(np.int32)
+    kb = [torch.from_numpy(np.ascontiguousarray(cuts[:, k])).cuda() for k in range(N)]
+    ke = [torch.from_numpy(np.ascontiguousarray(cuts[:, k + 1])).cuda() for k in range(N)]
+    part_out = torch.empty((batch.B * N * batch.q_chunk, batch.H, 512), dtype=torch.float32, device="cuda")
+    part_lse = torch.empty((batch.B * N * batch.q_chunk, batch.H), dtype=torch.float32, device="cuda")
+    indptr = torch.arange(0, (batch.B + 1) * N, N, dtype=torch.int32, device="cuda")
+    out, lse = db.alloc_outputs()
+    ws = db.workspace()
+    desc = db.desc()
+    stream = torch.cuda.current_stream()
+
+    def sharded_step(ev=None):
+        for k in range(N):
+            if ev is not None:
+                ev[k].record(stream)
+            B.splash_mla_attend_shard(db.q, db.kv, db.block_table, db.seq_lens, db.q_chunk, kb[k], ke[k], N, k,
+                                      part_out, part_lse, desc, ws, stream)
+        if ev is not None:
+            ev[N].record(stream)
+        B.splash_mla_combine(part_out, part_lse, indptr, batch.B, batch.q_chunk, batch.H, out, lse, stream)
+        if ev is not None:
+            ev[N + 1].record(stream)
+
+    t_w = time.perf_counter()
+    warmup_run = 0
+    while warmup_run < args.warmup or ((time.perf_counter() - t_w) * 1e3 < args.min_warmup_ms and warmup_run < 5000):
+        sharded_step()
+        warmup_run += 1
+        if warmup_run % 10 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        sharded_step()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t_start) * 1e3 / args.steps
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(N + 2)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        sharded_step(events[k])
+    torch.cuda.synchronize()
+    per_shard = np.array([[e[k].elapsed_time(e[k + 1]) for k in range(N)] for e in events]).mean(axis=0)
+    merge_ms = float(np.mean([e[N].elapsed_time(e[N + 1]) for e in events]))
+    shard_s = float(per_shard.sum()) * 1e-3
+
+    kv_bytes, alg_bytes, flops = W.workload_bytes_flops(batch)
+    hbm_time = alg_bytes / (HBM_PEAK_GBPS * 1e9)
+    mfma_time = flops / (BF16_PEAK_TFLOPS * 1e12)
+    if hbm_time >= mfma_time:
+        achieved = alg_bytes / shard_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4)}
+    else:
+        achieved = flops / shard_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4)}
+    roof.update({"traffic": None, "kernel": f"splash_mla_attend_shard x {N} (plan, attend and the shard's combine "
+                                            f"each), timed together",
+                 "kernel_avg_us": round(shard_s * 1e6, 2), "roofline_us": round(max(hbm_time, mfma_time) * 1e6, 1)})
+    result = {
+        "metric": METRIC + ", position-sharded",
+        "value": round(ms_per_step * 1e3, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "warmup_run": warmup_run,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded PCG64 draws of the workload's length mix; N(0,1) cache rows and queries)",
+        "config": {"workload": spec.name, "B": batch.B, "H": batch.H, "q_chunk": batch.q_chunk,
+                   "kv_cache": "fp8-e4m3+fp32 scale" if batch.kv_dtype else "bf16", "seed": spec.seed,
+                   "shards": N, "shard_cuts": "history b cut at floor(s_b k / N) rounded down to a page, k < N"},
+        "phases_us": {"shards": [round(float(x) * 1e3, 2) for x in per_shard], "merge": round(merge_ms * 1e3, 2)},
+        "roofline": roof,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -103,6 +197,9 @@ def main():
                     help="extra steps, each after a 1 GiB write that evicts L2 and MALL (reported separately)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--shards", type=int, default=0,
+                    help="position-sharded variant: cut every history into this many page-aligned shards, "
+                         "run splash_mla_attend_shard per shard and splash_mla_combine over them")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -124,6 +221,8 @@ def main():
     batch = W.make_config(args.config)
     log(f"workload {spec.name}: generated in {time.perf_counter() - t0:.1f} s")
     db = to_device(batch)
+    if args.shards > 0:
+        return run_sharded(args, spec, batch, db)
     out, lse = db.alloc_outputs()
     ws = db.workspace()
     desc = db.desc()

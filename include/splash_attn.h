@@ -164,6 +164,36 @@ int splash_mla_combine_splits(int32_t q_chunk, void* out, float* lse, const spla
                               void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * splash_mla_attend_shard: the partial result of one position shard (App. D,
+ * position-sharded CP: each rank holds a slice of a request's token history,
+ * and the ranks' partial results are merged by their log-sum-exp).  For every
+ * query row n = b*q_chunk + i and head h it attends over the keys of request
+ * b in [key_begin[b], key_end[b]) that row n sees (j <= seq_lens[b] - q_chunk
+ * + i), and writes the normalised fp32 output and its natural-log LSE into
+ * slot b*num_shards + shard:
+ *   part_out  fp32 [B*num_shards, q_chunk, H, 512]: rows of request b, shard k
+ *             at slot b*num_shards + k (this call writes its shard's slots)
+ *   part_lse  fp32 [B*num_shards, q_chunk, H]
+ * A row that sees no key of the shard gets out = 0 and lse = -inf.  After the
+ * num_shards calls (any order, same workspace reused), splash_mla_combine
+ * with split_indptr[b] = b*num_shards merges them into the result over the
+ * union of the shards: with shards that tile [0, seq_len) it equals
+ * splash_mla_attend.
+ *   key_begin, key_end  device int32 [B]; key_begin[b] a multiple of 64 (the
+ *             shard starts on a page), 0 <= key_begin[b] <= key_end[b]; only
+ *             the block-table entries of the shard's pages are read.
+ * The workspace needs a partial slot per query row (max_partials >= B *
+ * q_chunk, else SPLASH_ERR_WORKSPACE_TOO_SMALL).  Other arguments as for
+ * splash_mla_attend; SPLASH_FLAG_FORCE_SPLIT is rejected (UNSUPPORTED), and
+ * SPLASH_FLAG_DEBUG_CHECK also checks the key ranges.
+ */
+int splash_mla_attend_shard(const void* q, const void* kv_pages, const int32_t* block_table,
+                            const int32_t* seq_lens, int32_t q_chunk, const int32_t* key_begin,
+                            const int32_t* key_end, int32_t num_shards, int32_t shard, float* part_out,
+                            float* part_lse, const splash_mla_desc* desc, void* workspace,
+                            size_t ws_bytes, void* stream);
+
+/*
  * splash_mla_combine: merge partial attention results over disjoint key sets
  * into the result over their union (the merge a position-sharded history
  * needs, App. D).  For request b, partial slots s in

@@ -70,6 +70,8 @@ _SIGNATURES = {
     "splash_mla_attend_units": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine_splits": (ctypes.c_int, [_I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP]),
+    "splash_mla_attend_shard": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _I32, _I32, _VP, _VP, _PD, _VP,
+                                               _SZ, _VP]),
     "splash_mla_debug_gather": (ctypes.c_int, [_VP, _VP, _VP, _PD, _VP, _VP]),
     "splash_mla_plan_host": (ctypes.c_int, [_PI32, _I32, _PD, _I32, _I32, _PI32, _I32, _PI32, _PI32, _PI32]),
     "splash_mla_max_units": (_I32, [_I32, _I32, _I32]),
@@ -187,6 +189,15 @@ def splash_mla_attend_units(q, kv_pages, block_table, seq_lens, q_chunk: int, ou
 def splash_mla_combine_splits(q_chunk: int, out, lse, desc: MlaDesc, workspace, stream=None) -> None:
     _check(lib().splash_mla_combine_splits(q_chunk, _ptr(out), _ptr(lse), ctypes.byref(desc), _ptr(workspace),
                                            workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_attend_shard(q, kv_pages, block_table, seq_lens, q_chunk: int, key_begin, key_end,
+                            num_shards: int, shard: int, part_out, part_lse, desc: MlaDesc, workspace,
+                            stream=None) -> None:
+    _check(lib().splash_mla_attend_shard(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
+                                         _ptr(key_begin), _ptr(key_end), num_shards, shard, _ptr(part_out),
+                                         _ptr(part_lse), ctypes.byref(desc), _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def splash_mla_combine(partials, partial_lse, split_indptr, batch: int, q_chunk: int, num_heads: int,

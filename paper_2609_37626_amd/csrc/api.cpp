@@ -153,10 +153,19 @@ int prepare(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* d, 
   return SPLASH_OK;
 }
 
+// One position shard of every request's history (splash_mla_attend_shard);
+// all null for the whole history.
+struct Shard {
+  const int32_t* key_begin = nullptr;
+  const int32_t* key_end = nullptr;
+  int32_t num_shards = 0, shard = 0;
+};
+
 int check_device_data(const int32_t* block_table, const int32_t* seq_lens, int32_t q_chunk,
-                      const splash_mla_desc* d, const Workspace& wv, hipStream_t s) {
+                      const splash_mla_desc* d, const Workspace& wv, hipStream_t s, const Shard& sh = Shard()) {
   int32_t* res = wv.header + kHdrDebug;
-  hipError_t e = launch_check(block_table, seq_lens, d->batch, q_chunk, d->max_pages_per_seq, d->num_pages, res, s);
+  hipError_t e = launch_check(block_table, seq_lens, sh.key_begin, sh.key_end, d->batch, q_chunk,
+                              d->max_pages_per_seq, d->num_pages, res, s);
   if (e != hipSuccess) return hip_fail(e, "check launch");
   int32_t host = 0;
   e = hipMemcpyAsync(&host, res, sizeof host, hipMemcpyDeviceToHost, s);
@@ -164,18 +173,21 @@ int check_device_data(const int32_t* block_table, const int32_t* seq_lens, int32
   if (e != hipSuccess) return hip_fail(e, "check readback");
   if (host != INT32_MAX)
     return fail(SPLASH_ERR_INVALID_ARGUMENT,
-                "request %d: seq_len < q_chunk, history longer than the block-table row, or a block-table "
-                "entry outside [0, num_pages)",
+                "request %d: seq_len < q_chunk, history longer than the block-table row, a block-table "
+                "entry outside [0, num_pages), or (shard) a key range that is not 0 <= begin <= end with begin "
+                "a multiple of 64",
                 host - 1);
   return SPLASH_OK;
 }
 
 int do_plan(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* d, const Workspace& wv,
-            hipStream_t s) {
+            hipStream_t s, const Shard& sh = Shard()) {
   const int32_t G = device_workers();
   if (G < 1) return fail(SPLASH_ERR_HIP, "cannot query the device's compute units");
   PlanLaunch p;
   p.seq_lens = seq_lens;
+  p.key_begin = sh.key_begin;
+  p.key_end = sh.key_end;
   p.B = d->batch;
   p.q_chunk = q_chunk;
   p.G = G;
@@ -187,7 +199,7 @@ int do_plan(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* d, 
 
 int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens,
                     int32_t q_chunk, void* out, float* lse, const splash_mla_desc* d, const Workspace& wv,
-                    hipStream_t s) {
+                    hipStream_t s, const Shard& sh = Shard()) {
   const int32_t G = device_workers();
   if (G < 1) return fail(SPLASH_ERR_HIP, "cannot query the device's compute units");
   AttendLaunch a;
@@ -196,6 +208,8 @@ int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_ta
   a.kv_scales = d->kv_scales;
   a.block_table = block_table;
   a.seq_lens = seq_lens;
+  a.key_begin = sh.key_begin;
+  a.key_end = sh.key_end;
   a.out = out;
   a.lse = lse;
   a.bt_stride = d->max_pages_per_seq;
@@ -210,7 +224,7 @@ int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_ta
 }
 
 int do_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_desc* d, const Workspace& wv,
-                      hipStream_t s) {
+                      hipStream_t s, const Shard& sh = Shard()) {
   CombineLaunch c;
   c.partials = wv.part_out;
   c.partial_lse = wv.part_lse;
@@ -223,7 +237,11 @@ int do_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_d
   c.H = d->num_heads;
   c.out = out;
   c.out_lse = lse;
-  c.write_empty = false;
+  c.write_empty = sh.key_end != nullptr;  // a shard lists its tiles with no key, to be written empty
+  c.out_f32 = sh.key_end != nullptr;
+  c.num_shards = sh.key_end ? sh.num_shards : 0;
+  c.shard = sh.shard;
+  c.tile_q = q_chunk;
   hipError_t e = launch_combine(c, s);
   return e == hipSuccess ? SPLASH_OK : hip_fail(e, "combine launch");
 }
@@ -345,6 +363,43 @@ int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_
   return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
 }
 
+int splash_mla_attend_shard(const void* q, const void* kv_pages, const int32_t* block_table,
+                            const int32_t* seq_lens, int32_t q_chunk, const int32_t* key_begin,
+                            const int32_t* key_end, int32_t num_shards, int32_t shard, float* part_out,
+                            float* part_lse, const splash_mla_desc* desc, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if (!key_begin || !key_end || !part_lse)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "key_begin, key_end and part_lse must be non-NULL");
+  if (num_shards < 1 || shard < 0 || shard >= num_shards)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "need 0 <= shard < num_shards (got %d of %d)", shard, num_shards);
+  if (desc->flags & SPLASH_FLAG_FORCE_SPLIT)
+    return fail(SPLASH_ERR_UNSUPPORTED, "FORCE_SPLIT does not apply to a shard");
+  if ((st = check_tensors(q, kv_pages, block_table, part_out, part_lse)) != SPLASH_OK) return st;
+  Workspace wv;
+  if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
+  const int64_t T = (int64_t)desc->batch * q_chunk;
+  if (wv.max_partials < T)
+    return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL,
+                "a shard needs a partial slot for every query row: %lld, the workspace has %d", (long long)T,
+                wv.max_partials);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Shard sh;
+  sh.key_begin = key_begin;
+  sh.key_end = key_end;
+  sh.num_shards = num_shards;
+  sh.shard = shard;
+  if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
+    if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s, sh)) != SPLASH_OK) return st;
+  if ((st = do_plan(seq_lens, q_chunk, desc, wv, s, sh)) != SPLASH_OK) return st;
+  if ((st = do_attend_units(q, kv_pages, block_table, seq_lens, q_chunk, part_out, part_lse, desc, wv, s, sh)) !=
+      SPLASH_OK)
+    return st;
+  return do_combine_splits(q_chunk, part_out, part_lse, desc, wv, s, sh);
+}
+
 int splash_mla_combine(const float* partials, const float* partial_lse, const int32_t* split_indptr, int32_t batch,
                        int32_t q_chunk, int32_t num_heads, void* out, float* out_lse, void* stream) {
   if (batch < 0 || q_chunk < 1 || num_heads < 1)
@@ -367,6 +422,10 @@ int splash_mla_combine(const float* partials, const float* partial_lse, const in
   c.out = out;
   c.out_lse = out_lse;
   c.write_empty = true;
+  c.out_f32 = false;
+  c.num_shards = 0;
+  c.shard = 0;
+  c.tile_q = 1;
   hipError_t e = launch_combine(c, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SPLASH_OK : hip_fail(e, "combine launch");
 }

@@ -90,9 +90,16 @@ __device__ __forceinline__ float wave_xor32(float v) { return __shfl_xor(v, 32, 
 
 // ============================================================== planner ===
 
-__device__ __forceinline__ int32_t dev_tile_pages(const int32_t* seq_lens, int32_t q_chunk, int32_t t) {
+// Pages of tile t: its whole causal prefix, or under a shard its keys in
+// [key_begin[b], min(prefix, key_end[b])) (key_begin a page boundary).
+__device__ __forceinline__ int32_t dev_tile_pages(const int32_t* seq_lens, int32_t q_chunk, int32_t t,
+                                                  const int32_t* key_begin, const int32_t* key_end) {
   int32_t b = t / q_chunk, i = t - b * q_chunk;
   int32_t L = tile_keys(seq_lens[b], q_chunk, i);
+  if (key_end) {
+    const int32_t hi = min(L, key_end[b]), lo = key_begin[b];
+    return hi > lo ? ceil_div(hi, kPage) - lo / kPage : 0;
+  }
   return L > 0 ? ceil_div(L, kPage) : 0;
 }
 
@@ -186,16 +193,20 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t T = p.B * p.q_chunk;
   const bool cached = T <= kPlanLdsTiles;
+  // A shard's result is always a partial: every unit writes a partial slot
+  // (the combine turns each tile's parts into its fp32 result), and tiles
+  // with no key in the shard are listed for the combine with no parts.
+  const bool shard = p.key_end != nullptr;
   int32_t* hdr = p.ws.header;
   auto pages_of = [&](int32_t t) -> int32_t {
-    return cached ? s_pages[t] : dev_tile_pages(p.seq_lens, p.q_chunk, t);
+    return cached ? s_pages[t] : dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end);
   };
 
   // 1. page counts (cached), total and largest tile.
   int64_t tot = 0;
   int32_t mx = 0;
   for (int32_t t = tid; t < T; t += 1024) {
-    const int32_t P = dev_tile_pages(p.seq_lens, p.q_chunk, t);
+    const int32_t P = dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end);
     if (cached) s_pages[t] = P;
     tot += P;
     mx = P > mx ? P : mx;
@@ -271,13 +282,13 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       auto count = [&](int32_t P) {
         const int32_t n = (int32_t)udiv((uint32_t)(P + ck - 1), ud);  // ceil(P / c)
         W += n;
-        S += n > 1 ? n : 0;
+        S += (n > 1 || shard) ? n : 0;
       };
       if (cached) {
 #pragma unroll 4
         for (int32_t t = slice; t < T; t += nsl) count(s_pages[t]);
       } else {
-        for (int32_t t = slice; t < T; t += nsl) count(dev_tile_pages(p.seq_lens, p.q_chunk, t));
+        for (int32_t t = slice; t < T; t += nsl) count(dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end));
       }
       s_w[slice][j] = W;
       s_s[slice][j] = S;
@@ -321,7 +332,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   // max(16 C + U, max_{j < nl(C)} v_j - 16 C) with v_j = 16 (q_j + q_{G-1-j})
   // + U + U [q_{G-1-j} > 0] independent of C, so a running max of v over j
   // and a binary search for nl(C) = #{r : q_r > C} price a cap in O(log G).
-  bool fold = p.forced_chunk == 0 &&
+  bool fold = p.forced_chunk == 0 && !shard &&
               fold_applicable(T, p.G, kMaxWorkers, max_pages, total_pages, s_best, kPlanCosts);  // uniform
   int32_t cap = 0, nl = 0;
   if (fold) {
@@ -394,7 +405,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       *sp = P > cap ? 2 : 0;
     } else {
       *n = P > 0 ? ceil_div(P, c) : 0;
-      *sp = *n > 1 ? *n : 0;
+      *sp = (*n > 1 || shard) ? *n : 0;
     }
   };
 
@@ -405,7 +416,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     const int32_t P = t < T ? pages_of(t) : 0;
     int32_t n = 0, sp = 0;
     if (t < T) tile_units(t, P, &n, &sp);
-    const int32_t f = sp > 0 ? 1 : 0;
+    const int32_t f = (sp > 0 || (shard && t < T && P == 0)) ? 1 : 0;
     int32_t tu, ts, tf;
     const int32_t eu = block_exclusive_scan(n, s_scan, &tu) + carry_u;
     const int32_t es = block_exclusive_scan(sp, s_scan, &ts) + carry_s;
@@ -420,7 +431,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
           rec.x = t;
           rec.y = unit_begin(P, n, u);
           rec.z = unit_begin(P, n, u + 1);
-          rec.w = n > 1 ? es + u : -1;
+          rec.w = (n > 1 || shard) ? es + u : -1;
           p.ws.units[eu + u] = rec;
         }
       }
@@ -481,7 +492,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       rec.x = t;
       rec.y = unit_begin(P, n, u);
       rec.z = unit_begin(P, n, u + 1);
-      rec.w = n > 1 ? es + u : -1;
+      rec.w = (n > 1 || shard) ? es + u : -1;
       return rec;
     };
     const bool lpt = NU > p.G;  // uniform
@@ -799,12 +810,19 @@ void attend_kernel(AttendLaunch a) {
     __syncthreads();
     const int4 unit = s_unit;
     if (unit.x < 0) break;
-    const int tile = unit.x, p0 = unit.y, p1 = unit.z, slot = unit.w;
+    const int tile = unit.x, slot = unit.w;
     // The explicit vmcnt waits below assume every older memory operation of
     // this wave has completed (stores may complete out of order with loads).
     wait_vmcnt<0>();
     const int b = tile / a.q_chunk, qi = tile - b * a.q_chunk;
-    const int Lk = tile_keys(a.seq_lens[b], a.q_chunk, qi);
+    int Lk = tile_keys(a.seq_lens[b], a.q_chunk, qi);
+    int p0 = unit.y, p1 = unit.z;
+    if (a.key_end) {  // a shard: its pages count from the shard's first page
+      const int first = a.key_begin[b] >> 6;
+      p0 += first;
+      p1 += first;
+      Lk = min(Lk, a.key_end[b]);
+    }
     const int key_begin = p0 * kPage;
     const int key_end = min(p1 * kPage, Lk);
     const int nsteps = (key_end - key_begin + kStepKeys - 1) / kStepKeys;
@@ -1215,62 +1233,78 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
   const int64_t total = nreq * per_req;
   if (total == 0) return;
   const size_t stride = (size_t)c.q_chunk * c.H;  // between parts
-  if (c.item_list && c.max_parts && *c.max_parts <= kCombineRowParts) {
-    // Every listed item has at most kCombineRowParts parts: one wave per
-    // (item, row, head) with 8 columns per lane, every part's LSE and columns
-    // loaded at once, so each row costs two round trips to memory (its record,
-    // then the data) and no cross-lane reduction.
-    const int64_t per_item = (int64_t)c.q_chunk * c.H;
-    for (int64_t item = wave_global; item < nreq * per_item; item += nwaves) {
-      const int64_t ri = item / per_item;
-      const int row = (int)(item - ri * per_item);
-      const int qi = row / c.H, hh = row - qi * c.H;
-      const int4 rec = c.item_list[ri];
-      const int b = rec.x, s0 = rec.y, np = rec.z;
-      const size_t base = (size_t)qi * c.H + hh;
-      const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;
-      const float* plse = c.partial_lse + base;
-      const float* prow = c.partials + base * kDimV + 8 * lane;
-      f32x4 v[kCombineRowParts][2];
-      float w[kCombineRowParts];
+  // output row of (item b, chunk row qi): b * q_chunk + qi, or its place
+  // among the shards
+  auto out_row = [&](int b, int qi) -> size_t {
+    const size_t r = (size_t)b * c.q_chunk + qi;
+    if (c.num_shards <= 0) return r;
+    const size_t rb = r / (size_t)c.tile_q, ri = r - rb * (size_t)c.tile_q;
+    return (rb * c.num_shards + c.shard) * c.tile_q + ri;
+  };
+  // One wave per (item, row, head) with at most kCombineRowParts parts: 8
+  // columns per lane, every part's LSE and columns loaded at once, so the row
+  // costs one round trip to memory for its data and no cross-lane reduction.
+  auto row_merge = [&](int b, int s0, int np, int qi, int hh) {
+    const size_t base = (size_t)qi * c.H + hh;
+    const size_t orow = out_row(b, qi) * c.H + hh;
+    const float* plse = c.partial_lse + base;
+    const float* prow = c.partials + base * kDimV + 8 * lane;
+    f32x4 v[kCombineRowParts][2];
+    float w[kCombineRowParts];
+#pragma unroll
+    for (int u = 0; u < kCombineRowParts; ++u) {
+      w[u] = -INFINITY;
+      v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      if (u < np) {  // uniform
+        w[u] = plse[(size_t)(s0 + u) * stride];
+        const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
+        v[u][0] = src[0];
+        v[u][1] = src[1];
+      }
+    }
+    float M = -INFINITY, wsum = 0.f;
+#pragma unroll
+    for (int u = 0; u < kCombineRowParts; ++u) M = fmaxf(M, w[u]);
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    if (M > -INFINITY) {
 #pragma unroll
       for (int u = 0; u < kCombineRowParts; ++u) {
-        w[u] = -INFINITY;
-        v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        if (u < np) {  // uniform
-          w[u] = plse[(size_t)(s0 + u) * stride];
-          const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
-          v[u][0] = src[0];
-          v[u][1] = src[1];
-        }
+        const float wu = __expf(w[u] - M);  // 0 past the last part
+        wsum += wu;
+        acc0 += wu * v[u][0];
+        acc1 += wu * v[u][1];
       }
-      float M = -INFINITY, wsum = 0.f;
-#pragma unroll
-      for (int u = 0; u < kCombineRowParts; ++u) M = fmaxf(M, w[u]);
-      f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-      if (M > -INFINITY) {
-#pragma unroll
-        for (int u = 0; u < kCombineRowParts; ++u) {
-          const float wu = __expf(w[u] - M);  // 0 past the last part
-          wsum += wu;
-          acc0 += wu * v[u][0];
-          acc1 += wu * v[u][1];
-        }
-      }
-      const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    }
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    if (c.out_f32) {
+      f32x4* dst = (f32x4*)((float*)c.out + orow * kDimV + 8 * lane);
+      dst[0] = acc0 * inv;
+      dst[1] = acc1 * inv;
+    } else {
       u32x4 o4;
       o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
       o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
       o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
       o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
       *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
-      if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+    }
+    if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+  };
+  if (c.item_list && c.max_parts && *c.max_parts <= kCombineRowParts) {
+    // every listed item has at most kCombineRowParts parts
+    const int64_t per_item = (int64_t)c.q_chunk * c.H;
+    for (int64_t item = wave_global; item < nreq * per_item; item += nwaves) {
+      const int64_t ri = item / per_item;
+      const int row = (int)(item - ri * per_item);
+      const int qi = row / c.H, hh = row - qi * c.H;
+      const int4 rec = c.item_list[ri];
+      row_merge(rec.x, rec.y, rec.z, qi, hh);
     }
     return;
   }
   // one (request or tile, row, head, quarter) item
   auto combine_item = [&](int b, int s0, int s1, int quarter, int qi, int hh) {
-    const size_t orow = ((size_t)b * c.q_chunk + qi) * c.H + hh;
+    const size_t orow = out_row(b, qi) * c.H + hh;
     const int nparts = s1 - s0;
     const size_t base = (size_t)qi * c.H + hh;
     const float* plse = c.partial_lse + base;
@@ -1341,9 +1375,31 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
       }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    *(unsigned*)((uint16_t*)c.out + orow * kDimV + col) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+    if (c.out_f32)
+      *(f32x2*)((float*)c.out + orow * kDimV + col) = acc * inv;
+    else
+      *(unsigned*)((uint16_t*)c.out + orow * kDimV + col) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     if (lane == 0 && quarter == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
   };
+  if (!c.item_list) {
+    // by indptr (the standalone merge): one wave per (request, row, head),
+    // which takes the one-round-trip row merge when the request has at most
+    // kCombineRowParts parts and otherwise the four quarters in turn
+    const int64_t per_b = (int64_t)c.q_chunk * c.H;
+    for (int64_t item = wave_global; item < (int64_t)c.B * per_b; item += nwaves) {
+      const int b = (int)(item / per_b);
+      const int row = (int)(item - (int64_t)b * per_b);
+      const int qi = row / c.H, hh = row - qi * c.H;
+      const int s0 = c.indptr[b], s1 = c.indptr[b + 1];
+      if (s1 <= s0 && !c.write_empty) continue;
+      if (s1 - s0 <= kCombineRowParts) {
+        row_merge(b, s0, s1 - s0, qi, hh);
+      } else {
+        for (int quarter = 0; quarter < kCombineQuarters; ++quarter) combine_item(b, s0, s1, quarter, qi, hh);
+      }
+    }
+    return;
+  }
   for (int64_t item = wave_global; item < total; item += nwaves) {
     const int64_t ri = item / per_req;
     const int rem = (int)(item - ri * per_req);
@@ -1392,16 +1448,25 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint8_t* kv, const in
 // ================================================================ check ===
 //
 // Validates device data: q_chunk <= seq_lens[b] and every used block-table
-// entry in [0, num_pages).  Writes the smallest failing request + 1 (or 0).
-__global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int32_t* seq_lens, int32_t B,
+// entry in [0, num_pages); under a shard also 0 <= key_begin[b] <= key_end[b]
+// with key_begin[b] a page boundary, and only the shard's pages are used.
+// Writes the smallest failing request + 1 (or 0).
+__global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int32_t* seq_lens,
+                                                    const int32_t* key_begin, const int32_t* key_end, int32_t B,
                                                     int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
                                                     int32_t* result) {
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
     const int s = seq_lens[b];
     bool bad = s < q_chunk || (int64_t)(s + kPage - 1) / kPage > bt_stride;
-    if (!bad) {
-      const int np = (s + kPage - 1) / kPage;
-      for (int k = threadIdx.x; k < np; k += blockDim.x) {
+    int lo = 0, hi = s;
+    if (key_end) {
+      lo = key_begin[b];
+      hi = min(s, key_end[b]);
+      bad = bad || lo < 0 || (lo & (kPage - 1)) != 0 || key_end[b] < lo;
+    }
+    if (!bad && hi > lo) {
+      const int np = (hi + kPage - 1) / kPage;
+      for (int k = lo / kPage + threadIdx.x; k < np; k += blockDim.x) {
         const int v = bt[(size_t)b * bt_stride + k];
         if (v < 0 || v >= num_pages) bad = true;
       }
@@ -1443,12 +1508,13 @@ hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_l
   return hipGetLastError();
 }
 
-hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, int32_t B, int32_t q_chunk, int32_t bt_stride,
-                        int32_t num_pages, int32_t* result, hipStream_t s) {
+hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* key_begin,
+                        const int32_t* key_end, int32_t B, int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
+                        int32_t* result, hipStream_t s) {
   hipLaunchKernelGGL(init_check, dim3(1), dim3(1), 0, s, result);
   int blocks = B < 1024 ? B : 1024;
-  hipLaunchKernelGGL(check_kernel, dim3(blocks), dim3(256), 0, s, bt, seq_lens, B, q_chunk, bt_stride, num_pages,
-                     result);
+  hipLaunchKernelGGL(check_kernel, dim3(blocks), dim3(256), 0, s, bt, seq_lens, key_begin, key_end, B, q_chunk,
+                     bt_stride, num_pages, result);
   return hipGetLastError();
 }
 

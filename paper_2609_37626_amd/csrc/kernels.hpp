@@ -38,6 +38,8 @@ enum HeaderSlot : int {
 
 struct PlanLaunch {
   const int32_t* seq_lens;
+  const int32_t* key_begin;  // shard: request b's keys [key_begin[b], key_end[b]) (nullptr: whole history)
+  const int32_t* key_end;
   int32_t B, q_chunk, G, forced_chunk;
   Workspace ws;
 };
@@ -48,6 +50,8 @@ struct AttendLaunch {
   const float* kv_scales;
   const int32_t* block_table;
   const int32_t* seq_lens;
+  const int32_t* key_begin;  // shard (see PlanLaunch): unit pages count from key_begin[b] / 64
+  const int32_t* key_end;
   void* out;
   float* lse;
   int32_t bt_stride, q_chunk, H, kv_dtype, B;
@@ -67,6 +71,9 @@ struct CombineLaunch {
   void* out;
   float* out_lse;
   bool write_empty;          // requests without partials get out = 0, lse = -inf
+  bool out_f32;              // out is fp32 (a shard's partial result) instead of bf16
+  int32_t num_shards, shard, tile_q;  // num_shards > 0: output row r = b' * tile_q + i goes to row
+                                      // (b' * num_shards + shard) * tile_q + i
 };
 
 hipError_t launch_plan(const PlanLaunch& p, hipStream_t s);
@@ -74,7 +81,8 @@ hipError_t launch_attend(const AttendLaunch& p, int32_t workers, hipStream_t s);
 hipError_t launch_combine(const CombineLaunch& p, hipStream_t s);
 hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_lens, int32_t B,
                          int32_t bt_stride, int32_t row_bytes, void* dense, hipStream_t s);
-hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, int32_t B, int32_t q_chunk,
-                        int32_t bt_stride, int32_t num_pages, int32_t* result, hipStream_t s);
+hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* key_begin,
+                        const int32_t* key_end, int32_t B, int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
+                        int32_t* result, hipStream_t s);
 
 }  // namespace splash

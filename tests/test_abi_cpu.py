@@ -107,6 +107,27 @@ def test_idle_owner_is_a_noop_even_with_null_pointers():
     assert L.splash_mla_combine(None, None, None, 0, 1, 16, None, None, None) == B.SPLASH_OK
 
 
+def call_shard(desc, kb=FAKE, ke=FAKE, num_shards=2, shard=0, part_out=FAKE, part_lse=FAKE, ws_bytes=1 << 30):
+    L = B.lib()
+    return L.splash_mla_attend_shard(FAKE, FAKE, FAKE, FAKE, 1, kb, ke, num_shards, shard, part_out, part_lse,
+                                     ctypes.byref(desc), FAKE, ws_bytes, None)
+
+
+def test_shard_arguments_are_checked_before_the_device():
+    assert call_shard(good_desc(), kb=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_shard(good_desc(), ke=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_shard(good_desc(), part_lse=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_shard(good_desc(), shard=2) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_shard(good_desc(), shard=-1) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_shard(good_desc(), num_shards=0, shard=0) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert call_shard(good_desc(), part_out=FAKE + 4) == B.SPLASH_ERR_MISALIGNED
+    assert call_shard(good_desc(flags=B.FLAG_FORCE_SPLIT, split_pages=2)) == B.SPLASH_ERR_UNSUPPORTED
+    # a partial slot per query row: 4 rows need 4 slots
+    assert call_shard(good_desc(), ws_bytes=B.workspace_size(4, 1, 16, 3)) == B.SPLASH_ERR_WORKSPACE_TOO_SMALL
+    assert b"partial slot" in B.lib().splash_last_error()
+    assert call_shard(good_desc(batch=0), kb=0, ke=0, part_out=0, part_lse=0) == B.SPLASH_OK
+
+
 def test_status_strings():
     L = B.lib()
     for st in [0, -1, -2, -3, -4, -5]:
