@@ -88,6 +88,86 @@ def cpu_baseline(batch, budget_s):
             "cpu_threads_available": len(os.sched_getaffinity(0))}
 
 
+def run_dop(args, spec, batch):
+    """--dop-ranks T: one GPU's share of a layer's DOP regroup.  As a rank it
+    packs its H/T heads of all N rows by owner and later puts its output rows
+    back in order; as an owner it assembles its N/T rows (requests dealt out
+    round-robin) with all heads and splits its output by rank.  The
+    all-to-all between them is not timed (it is not part of the library)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37626_amd import binding as B
+
+    T = args.dop_ranks
+    N = args.dop_rows if args.dop_rows > 0 else batch.B * batch.q_chunk
+    H = batch.H
+    if H % T:
+        raise SystemExit(f"--dop-ranks {T} must divide the {H} heads")
+    hl = H // T
+    owner = (np.arange(N) // batch.q_chunk) % T                  # request b's rows go to owner b % T
+    order = np.concatenate([np.flatnonzero(owner == o) for o in range(T)]).astype(np.int32)
+    n_own = int(np.count_nonzero(owner == 0))
+    order_d = torch.from_numpy(order).cuda()
+    g = torch.Generator(device="cuda").manual_seed(spec.seed)
+    rnd = lambda *shape: torch.randint(-32768, 32767, shape, dtype=torch.int16, device="cuda", generator=g)
+    q_nope, q_rope = rnd(N, hl, 512), rnd(N, hl, 64)
+    send_q, recv_q, q_owner = rnd(N, hl, 576), rnd(T * n_own, hl, 576), rnd(n_own, H, 576)
+    out_owner, send_o, recv_o, out = rnd(n_own, H, 512), rnd(T * n_own, hl, 512), rnd(N, hl, 512), rnd(N, hl, 512)
+    stream = torch.cuda.current_stream()
+    kernels = [
+        ("pack_q", lambda: B.splash_dop_pack_q(q_nope, q_rope, order_d, send_q, stream), 2 * N * hl * 576 * 2),
+        ("unpack_q", lambda: B.splash_dop_unpack_q(recv_q, T, q_owner, stream), 2 * n_own * H * 576 * 2),
+        ("pack_out", lambda: B.splash_dop_pack_out(out_owner, T, send_o, stream), 2 * n_own * H * 512 * 2),
+        ("unpack_out", lambda: B.splash_dop_unpack_out(recv_o, order_d, out, stream), 2 * N * hl * 512 * 2),
+    ]
+
+    def layer():
+        for _, fn, _ in kernels:
+            fn()
+
+    t_w = time.perf_counter()
+    warm = 0
+    while warm < args.warmup or ((time.perf_counter() - t_w) * 1e3 < args.min_warmup_ms and warm < 20000):
+        layer()
+        warm += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(kernels) + 1)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        for i, (_, fn, _) in enumerate(kernels):
+            ev[k][i].record(stream)
+            fn()
+        ev[k][len(kernels)].record(stream)
+    torch.cuda.synchronize()
+    per = {name: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) * 1e3
+           for i, (name, _, _) in enumerate(kernels)}
+    gbps = {name: round(nbytes / (per[name] * 1e-6) / 1e9, 1) for name, _, nbytes in kernels}
+    total_bytes = sum(nb for _, _, nb in kernels)
+    dom = max(per, key=per.get)
+    dom_bytes = dict((n, nb) for n, _, nb in kernels)[dom]
+    achieved = dom_bytes / (per[dom] * 1e-6) / 1e9
+    result = {
+        "metric": "us per layer and GB/s of one GPU's DOP query + output regroup (pack, unpack; all-to-all not "
+                  "included)",
+        "value": round(ms * 1e3, 2), "unit": "us/layer", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (random bf16 bit patterns)",
+        "config": {"workload": spec.name, "ranks": T, "rows": N, "H": H, "heads_per_rank": hl,
+                   "rows_owned": n_own, "owner_of_request": "b mod ranks"},
+        "kernel_us": {k: round(v, 2) for k, v in per.items()}, "kernel_gbps": gbps,
+        "bytes_per_layer": total_bytes, "gbps_per_layer": round(total_bytes / (ms * 1e-3) / 1e9, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": f"dop {dom}",
+                     "kernel_avg_us": round(per[dom], 2), "alg_bytes_per_launch": dom_bytes},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def run_sharded(args, spec, batch, db):
     """--shards N: every history cut into N page-aligned position shards of
     (nearly) equal length; a step is the N shard calls (each: plan, attend,
@@ -197,6 +277,11 @@ def main():
                     help="extra steps, each after a 1 GiB write that evicts L2 and MALL (reported separately)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--dop-ranks", type=int, default=0,
+                    help="DOP regroup: time one GPU's share of a layer's query and output regroup for this many "
+                         "ranks (pack its head slice, assemble its own rows, and back)")
+    ap.add_argument("--dop-rows", type=int, default=0,
+                    help="with --dop-ranks: current query rows N (default: the workload's B * q_chunk)")
     ap.add_argument("--shards", type=int, default=0,
                     help="position-sharded variant: cut every history into this many page-aligned shards, "
                          "run splash_mla_attend_shard per shard and splash_mla_combine over them")
@@ -220,6 +305,8 @@ def main():
     t0 = time.perf_counter()
     batch = W.make_config(args.config)
     log(f"workload {spec.name}: generated in {time.perf_counter() - t0:.1f} s")
+    if args.dop_ranks > 0:
+        return run_dop(args, spec, batch)
     db = to_device(batch)
     if args.shards > 0:
         return run_sharded(args, spec, batch, db)

@@ -164,6 +164,44 @@ int splash_mla_combine_splits(int32_t q_chunk, void* out, float* lse, const spla
                               void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * DOP regroup (Sec. 3 "DOP: Computation"; App. E, DOP transfer).  With
+ * sharded projections, rank t of T holds all N current query rows for its
+ * heads_local = H/T heads (global heads [t*H/T, (t+1)*H/T)); the owner of a
+ * request needs that request's rows for all H heads.  A variable-size
+ * all-to-all (not part of this library; its split sizes are the per-owner
+ * row counts) moves one contiguous block between every pair.  These calls
+ * build and take apart those blocks; rows keep their identity, heads their
+ * order, and each packed query row carries the no-position part followed by
+ * the rotary part.  All tensors are bf16, contiguous, 16-byte aligned
+ * device buffers; row_order is a device int32 [num_rows] permutation of the
+ * rows, grouped by owner (owner 0's rows first); it is not validated.
+ *
+ * splash_dop_pack_q (rank side, before attention):
+ *   q_nope [num_rows, heads_local, 512], q_rope [num_rows, heads_local, 64]
+ *   -> send [num_rows, heads_local, 576], send[k] = q_nope[row_order[k]] | q_rope[row_order[k]]
+ * splash_dop_unpack_q (owner side): recv [num_ranks, owner_rows, heads_local,
+ *   576] (rank t's block t) -> q_owner [owner_rows, num_ranks*heads_local, 576],
+ *   q_owner[i][t*heads_local + h] = recv[t][i][h]
+ * splash_dop_pack_out (owner side, after attention): out_owner [owner_rows,
+ *   num_ranks*heads_local, 512] -> send [num_ranks, owner_rows, heads_local,
+ *   512], send[t][i][h] = out_owner[i][t*heads_local + h]
+ * splash_dop_unpack_out (rank side): recv [num_rows, heads_local, 512] in
+ *   row_order -> out [num_rows, heads_local, 512], out[row_order[k]] = recv[k]
+ *
+ * Zero rows is a no-op (an owner with no rows still takes part in the
+ * exchange).  Errors: INVALID_ARGUMENT for negative or zero sizes or NULL
+ * buffers, MISALIGNED, UNSUPPORTED when rows * H * 72 reaches 2^31.
+ */
+int splash_dop_pack_q(const void* q_nope, const void* q_rope, const int32_t* row_order,
+                      int32_t num_rows, int32_t heads_local, void* send, void* stream);
+int splash_dop_unpack_q(const void* recv, int32_t num_ranks, int32_t owner_rows,
+                        int32_t heads_local, void* q_owner, void* stream);
+int splash_dop_pack_out(const void* out_owner, int32_t num_ranks, int32_t owner_rows,
+                        int32_t heads_local, void* send, void* stream);
+int splash_dop_unpack_out(const void* recv, const int32_t* row_order, int32_t num_rows,
+                          int32_t heads_local, void* out, void* stream);
+
+/*
  * splash_mla_attend_shard: the partial result of one position shard (App. D,
  * position-sharded CP: each rank holds a slice of a request's token history,
  * and the ranks' partial results are merged by their log-sum-exp).  For every

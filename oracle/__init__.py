@@ -21,10 +21,11 @@ torch's float64 scaled-dot-product attention, closed forms, invariants, a
 hand-worked example, and the format definitions cross-checked with numpy and
 torch dtypes).
 """
+from . import dop
 from .formats import bf16_bits_to_f64, e4m3_bits_to_f64
 from .mla import (gather_history, mla_attention, mla_attention_sampled,
                   merge_partials, attention_rows)
 
-__all__ = ["bf16_bits_to_f64", "e4m3_bits_to_f64", "gather_history",
+__all__ = ["dop", "bf16_bits_to_f64", "e4m3_bits_to_f64", "gather_history",
            "mla_attention", "mla_attention_sampled", "merge_partials",
            "attention_rows"]

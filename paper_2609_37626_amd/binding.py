@@ -70,6 +70,10 @@ _SIGNATURES = {
     "splash_mla_attend_units": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine_splits": (ctypes.c_int, [_I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP]),
+    "splash_dop_pack_q": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _VP, _VP]),
+    "splash_dop_unpack_q": (ctypes.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
+    "splash_dop_pack_out": (ctypes.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
+    "splash_dop_unpack_out": (ctypes.c_int, [_VP, _VP, _I32, _I32, _VP, _VP]),
     "splash_mla_attend_shard": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _I32, _I32, _VP, _VP, _PD, _VP,
                                                _SZ, _VP]),
     "splash_mla_debug_gather": (ctypes.c_int, [_VP, _VP, _VP, _PD, _VP, _VP]),
@@ -198,6 +202,30 @@ def splash_mla_attend_shard(q, kv_pages, block_table, seq_lens, q_chunk: int, ke
                                          _ptr(key_begin), _ptr(key_end), num_shards, shard, _ptr(part_out),
                                          _ptr(part_lse), ctypes.byref(desc), _ptr(workspace),
                                          workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_dop_pack_q(q_nope, q_rope, row_order, send, stream=None) -> None:
+    """Rank side: send[k] = q_nope[row_order[k]] | q_rope[row_order[k]] (all local heads)."""
+    n, hl = int(q_nope.shape[0]), int(q_nope.shape[1])
+    _check(lib().splash_dop_pack_q(_ptr(q_nope), _ptr(q_rope), _ptr(row_order), n, hl, _ptr(send), _stream(stream)))
+
+
+def splash_dop_unpack_q(recv, num_ranks: int, q_owner, stream=None) -> None:
+    """Owner side: recv [T, n, H/T, 576] -> q_owner [n, H, 576]."""
+    n, H = int(q_owner.shape[0]), int(q_owner.shape[1])
+    _check(lib().splash_dop_unpack_q(_ptr(recv), num_ranks, n, H // num_ranks, _ptr(q_owner), _stream(stream)))
+
+
+def splash_dop_pack_out(out_owner, num_ranks: int, send, stream=None) -> None:
+    """Owner side: out_owner [n, H, 512] -> send [T, n, H/T, 512]."""
+    n, H = int(out_owner.shape[0]), int(out_owner.shape[1])
+    _check(lib().splash_dop_pack_out(_ptr(out_owner), num_ranks, n, H // num_ranks, _ptr(send), _stream(stream)))
+
+
+def splash_dop_unpack_out(recv, row_order, out, stream=None) -> None:
+    """Rank side: out[row_order[k]] = recv[k] (all local heads)."""
+    n, hl = int(out.shape[0]), int(out.shape[1])
+    _check(lib().splash_dop_unpack_out(_ptr(recv), _ptr(row_order), n, hl, _ptr(out), _stream(stream)))
 
 
 def splash_mla_combine(partials, partial_lse, split_indptr, batch: int, q_chunk: int, num_heads: int,

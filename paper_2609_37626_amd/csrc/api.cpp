@@ -263,6 +263,24 @@ int check_tensors(const void* q, const void* kv_pages, const int32_t* block_tabl
   return SPLASH_OK;
 }
 
+// ---- DOP regroup (sizes checked here; row_order is device data, a
+// permutation of [0, num_rows) grouped by owner, and is not checked)
+int dop_check(int64_t rows, int32_t hl, int32_t num_ranks, const void* const* ptrs, int nptr) {
+  if (rows < 0 || hl < 1 || num_ranks < 1)
+    return fail(SPLASH_ERR_INVALID_ARGUMENT, "need rows >= 0, heads_local >= 1, num_ranks >= 1");
+  if (rows * hl * num_ranks * 72 >= INT32_MAX)
+    return fail(SPLASH_ERR_UNSUPPORTED, "regroup too large (%lld rows)", (long long)rows);
+  if (rows == 0) return SPLASH_OK;
+  for (int i = 0; i < nptr; ++i) {
+    if (!ptrs[i]) return fail(SPLASH_ERR_INVALID_ARGUMENT, "NULL buffer");
+  }
+  for (int i = 0; i < nptr; ++i) {
+    if (i != 2 && !aligned16(ptrs[i]))  // slot 2, when used, is the int32 row order
+      return fail(SPLASH_ERR_MISALIGNED, "regroup buffers must be 16-byte aligned");
+  }
+  return SPLASH_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -586,6 +604,45 @@ int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const sp
     stats_out[6] = fold ? (nl > 0 ? 2 : 1) : (max_pages + c - 1) / c;
   }
   return SPLASH_OK;
+}
+
+int splash_dop_pack_q(const void* q_nope, const void* q_rope, const int32_t* row_order, int32_t num_rows,
+                      int32_t heads_local, void* send, void* stream) {
+  const void* ptrs[4] = {q_nope, q_rope, row_order, send};
+  int st = dop_check(num_rows, heads_local, 1, ptrs, 4);
+  if (st != SPLASH_OK || num_rows == 0) return st;
+  hipError_t e = launch_dop_pack_q(q_nope, q_rope, row_order, num_rows, heads_local, send,
+                                   static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "dop pack_q launch");
+}
+
+int splash_dop_unpack_q(const void* recv, int32_t num_ranks, int32_t owner_rows, int32_t heads_local, void* q_owner,
+                        void* stream) {
+  const void* ptrs[2] = {recv, q_owner};
+  int st = dop_check(owner_rows, heads_local, num_ranks, ptrs, 2);
+  if (st != SPLASH_OK || owner_rows == 0) return st;
+  hipError_t e = launch_dop_unpack_q(recv, num_ranks, owner_rows, heads_local, q_owner,
+                                     static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "dop unpack_q launch");
+}
+
+int splash_dop_pack_out(const void* out_owner, int32_t num_ranks, int32_t owner_rows, int32_t heads_local, void* send,
+                        void* stream) {
+  const void* ptrs[2] = {out_owner, send};
+  int st = dop_check(owner_rows, heads_local, num_ranks, ptrs, 2);
+  if (st != SPLASH_OK || owner_rows == 0) return st;
+  hipError_t e = launch_dop_pack_out(out_owner, num_ranks, owner_rows, heads_local, send,
+                                     static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "dop pack_out launch");
+}
+
+int splash_dop_unpack_out(const void* recv, const int32_t* row_order, int32_t num_rows, int32_t heads_local, void* out,
+                          void* stream) {
+  const void* ptrs[4] = {recv, out, row_order, out};
+  int st = dop_check(num_rows, heads_local, 1, ptrs, 4);
+  if (st != SPLASH_OK || num_rows == 0) return st;
+  hipError_t e = launch_dop_unpack_out(recv, row_order, num_rows, heads_local, out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SPLASH_OK : hip_fail(e, "dop unpack_out launch");
 }
 
 const char* splash_status_string(int status) {

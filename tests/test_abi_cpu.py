@@ -128,6 +128,19 @@ def test_shard_arguments_are_checked_before_the_device():
     assert call_shard(good_desc(batch=0), kb=0, ke=0, part_out=0, part_lse=0) == B.SPLASH_OK
 
 
+def test_dop_regroup_arguments_are_checked_before_the_device():
+    L = B.lib()
+    assert L.splash_dop_pack_q(None, None, None, 0, 16, None, None) == B.SPLASH_OK          # an idle rank
+    assert L.splash_dop_unpack_q(None, 8, 0, 16, None, None) == B.SPLASH_OK                # an idle owner
+    assert L.splash_dop_pack_q(FAKE, FAKE, FAKE, -1, 16, FAKE, None) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert L.splash_dop_pack_q(FAKE, FAKE, FAKE, 4, 0, FAKE, None) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert L.splash_dop_pack_q(FAKE, None, FAKE, 4, 16, FAKE, None) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert L.splash_dop_pack_q(FAKE, FAKE + 8, FAKE, 4, 16, FAKE, None) == B.SPLASH_ERR_MISALIGNED
+    assert L.splash_dop_unpack_q(FAKE, 0, 4, 16, FAKE, None) == B.SPLASH_ERR_INVALID_ARGUMENT
+    assert L.splash_dop_pack_out(FAKE, 8, 1 << 20, 128, FAKE, None) == B.SPLASH_ERR_UNSUPPORTED
+    assert L.splash_dop_unpack_out(FAKE, FAKE, 4, 16, FAKE + 2, None) == B.SPLASH_ERR_MISALIGNED
+
+
 def test_status_strings():
     L = B.lib()
     for st in [0, -1, -2, -3, -4, -5]:

@@ -272,3 +272,63 @@ def test_planted_mistake_is_caught(name):
     kind, fn = MUTANTS[name]
     with _planted(kind, fn):
         assert not _pins_all_pass(), f"no pin caught: {name}"
+
+
+# ------------------------------------------------------------ DOP regroup ---
+# Sec. 3 "DOP: Computation" and "Cost"; App. E, DOP transfer.
+
+def _dop_round_trip(N, H, T, owner_of_row, seed):
+    from oracle import dop
+    rng = np.random.default_rng(seed)
+    hl = H // T
+    q = rng.integers(0, 1 << 16, size=(N, H, 576), dtype=np.uint16)
+    out_full = rng.integers(0, 1 << 16, size=(N, H, 512), dtype=np.uint16)
+    order, off = dop.row_order(owner_of_row, T)
+    counts = np.diff(off)
+    # forward: every rank packs its head slice by owner, the all-to-all moves
+    # block o of every rank to owner o
+    send = [dop.pack_q(q[:, t * hl:(t + 1) * hl, :512], q[:, t * hl:(t + 1) * hl, 512:], order) for t in range(T)]
+    recv, moved_q = dop.exchange(send, [counts] * T)
+    for o in range(T):
+        rows = np.flatnonzero(np.asarray(owner_of_row) == o)       # ascending global rows of owner o
+        q_owner = dop.unpack_q(recv[o], T, len(rows))
+        assert q_owner.shape == (len(rows), H, 576)
+        assert np.array_equal(q_owner, q[rows])                     # all heads, in head order, rows kept
+    # reverse: every owner splits its [N_o, H, 512] by rank, rank t gets its
+    # heads of every row back in global row order
+    send_r = [dop.pack_out(out_full[np.flatnonzero(np.asarray(owner_of_row) == o)], T) for o in range(T)]
+    recv_r, moved_o = dop.exchange(send_r, [[counts[o]] * T for o in range(T)])
+    for t in range(T):
+        assert np.array_equal(dop.unpack_out(recv_r[t], order), out_full[:, t * hl:(t + 1) * hl])
+    return moved_q, moved_o
+
+
+@pytest.mark.parametrize("N,H,T,seed", [(13, 16, 4, 1), (256, 128, 8, 2), (5, 32, 8, 3)])
+def test_dop_regroup_round_trip_and_traffic(N, H, T, seed):
+    owner = np.random.default_rng(seed + 100).integers(0, T, size=N)
+    if T > 2:
+        owner[owner == 1] = 2                                        # an idle owner
+    moved_q, moved_o = _dop_round_trip(N, H, T, owner, seed)
+    # Sec. 3 "Cost": the two exchanges receive (1 - 1/T) N H (d_q + d_z) b
+    # bytes in aggregate, b = 2 (bf16), d_q = 576, d_z = 512
+    assert moved_q + moved_o == (T - 1) * N * H * (576 + 512) * 2 // T
+    assert moved_q == (T - 1) * N * H * 576 * 2 // T
+
+
+def test_dop_head_order_worked_example():
+    # two ranks, four heads, three rows; rows 0 and 2 belong to owner 1.  The
+    # owner's head 3 is rank 1's local head 1, and the rotary part follows the
+    # no-position part in each packed row.
+    from oracle import dop
+    q = np.zeros((3, 4, 576), dtype=np.uint16)
+    for n in range(3):
+        for h in range(4):
+            q[n, h] = 100 * n + 10 * h + np.arange(576) % 7
+    order, off = dop.row_order([1, 0, 1], 2)
+    assert order.tolist() == [1, 0, 2] and off.tolist() == [0, 1, 3]
+    send1 = dop.pack_q(q[:, 2:4, :512], q[:, 2:4, 512:], order)
+    assert np.array_equal(send1[0, 1], q[1, 3])                   # owner 0's row first, rank 1's local head 1
+    recv, _ = dop.exchange([dop.pack_q(q[:, 0:2, :512], q[:, 0:2, 512:], order), send1], [[1, 2], [1, 2]])
+    q1 = dop.unpack_q(recv[1], 2, 2)
+    assert q1[0, 3, 0] == 30 and q1[1, 2, 5] == 200 + 20 + 5   # row 0 head 3; row 2 head 2, dim 5
+    assert np.array_equal(q1[1, 3], q[2, 3]) and np.array_equal(q1[0, 0], q[0, 0])
