@@ -88,6 +88,92 @@ def cpu_baseline(batch, budget_s):
             "cpu_threads_available": len(os.sched_getaffinity(0))}
 
 
+def run_topk(args, spec, batch):
+    """--topk K: every row n attends min(K, visible) distinct positions of its
+    request's history, drawn uniformly (seeded) and listed in position order;
+    a step is one splash_mla_attend_topk call (plan, attend, combine)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37626_amd import binding as B
+    from paper_2609_37626_amd.device import to_device
+
+    K = args.topk
+    rng = np.random.Generator(np.random.PCG64(spec.seed + 1000))
+    N = batch.B * batch.q_chunk
+    idx = np.full((N, K), -1, dtype=np.int32)
+    cnt = np.zeros(N, dtype=np.int32)
+    for n in range(N):
+        b, i = divmod(n, batch.q_chunk)
+        vis = int(batch.seq_lens[b]) - batch.q_chunk + i + 1
+        c = min(K, vis)
+        idx[n, :c] = np.sort(rng.choice(vis, size=c, replace=False))
+        cnt[n] = c
+    db = to_device(batch)
+    out, lse = db.alloc_outputs()
+    ws = db.workspace()
+    desc = db.desc()
+    idx_d, cnt_d = torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda()
+    stream = torch.cuda.current_stream()
+
+    def step():
+        B.splash_mla_attend_topk(db.q, db.kv, db.block_table, db.seq_lens, batch.q_chunk, idx_d, cnt_d, out, lse,
+                                 desc, ws, stream)
+
+    t_w = time.perf_counter()
+    warm = 0
+    while warm < args.warmup or ((time.perf_counter() - t_w) * 1e3 < args.min_warmup_ms and warm < 5000):
+        step()
+        warm += 1
+        if warm % 10 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        step()
+        ev[k][1].record(stream)
+    torch.cuda.synchronize()
+    call_us = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
+
+    sel = int(cnt.sum())
+    row_bytes = 580 if batch.kv_dtype else 1152
+    H = batch.H
+    alg_bytes = sel * row_bytes + N * H * (576 * 2 + 512 * 2 + 4) + sel * 4
+    flops = 2.0 * H * (576 + 512) * sel
+    hbm_t, mfma_t = alg_bytes / (HBM_PEAK_GBPS * 1e9), flops / (BF16_PEAK_TFLOPS * 1e12)
+    if hbm_t >= mfma_t:
+        ach = alg_bytes / (call_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBPS, 4)}
+    else:
+        ach = flops / (call_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / BF16_PEAK_TFLOPS, 4)}
+    roof.update({"traffic": None, "kernel": "splash_mla_attend_topk (plan, attend, combine) timed together",
+                 "kernel_avg_us": round(call_us, 2), "alg_bytes_per_launch": int(alg_bytes),
+                 "alg_flops_per_launch": int(flops), "roofline_us": round(max(hbm_t, mfma_t) * 1e6, 1)})
+    result = {
+        "metric": METRIC + ", top-k",
+        "value": round(ms * 1e3, 2), "unit": "us/step", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "warmup_run": warm, "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded PCG64 draws of the workload's length mix; N(0,1) cache rows and queries; "
+                "uniform position choice)",
+        "config": {"workload": spec.name, "B": batch.B, "H": H, "q_chunk": batch.q_chunk,
+                   "kv_cache": "fp8-e4m3+fp32 scale" if batch.kv_dtype else "bf16", "seed": spec.seed, "topk": K,
+                   "selected_rows": sel},
+        "kv_gbps": round(sel * row_bytes / (ms * 1e-3) / 1e9, 1),
+        "roofline": roof,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def run_dop(args, spec, batch):
     """--dop-ranks T: one GPU's share of a layer's DOP regroup.  As a rank it
     packs its H/T heads of all N rows by owner and later puts its output rows
@@ -277,6 +363,9 @@ def main():
                     help="extra steps, each after a 1 GiB write that evicts L2 and MALL (reported separately)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--topk", type=int, default=0,
+                    help="top-k variant: every row attends this many of its visible positions (a seeded uniform "
+                         "choice, in position order) through splash_mla_attend_topk")
     ap.add_argument("--dop-ranks", type=int, default=0,
                     help="DOP regroup: time one GPU's share of a layer's query and output regroup for this many "
                          "ranks (pack its head slice, assemble its own rows, and back)")
@@ -307,6 +396,8 @@ def main():
     log(f"workload {spec.name}: generated in {time.perf_counter() - t0:.1f} s")
     if args.dop_ranks > 0:
         return run_dop(args, spec, batch)
+    if args.topk > 0:
+        return run_topk(args, spec, batch)
     db = to_device(batch)
     if args.shards > 0:
         return run_sharded(args, spec, batch, db)

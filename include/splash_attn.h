@@ -164,6 +164,31 @@ int splash_mla_combine_splits(int32_t q_chunk, void* out, float* lse, const spla
                               void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * splash_mla_attend_topk: top-k (sparse) attention, the attention the paper's
+ * sparse backend runs (each row attends a selected subset of its history,
+ * chosen by an indexer that is not part of this library).  Row n =
+ * b*q_chunk + i attends the token positions topk_idx[n][0 .. topk_count[n])
+ * of request b's history, with the logits, values, softmax and LSE of
+ * splash_mla_attend restricted to those keys:
+ *   topk_idx    device int32 [B*q_chunk, topk]: positions, each in the row's
+ *               visible prefix [0, seq_lens[b] - q_chunk + i]; entries past
+ *               the count are not read.  A position listed twice counts twice.
+ *   topk_count  device int32 [B*q_chunk], 0 <= count <= topk; a row with an
+ *               empty list gets out = 0, lse = -inf.
+ * Only the block-table entries of listed positions are read.  Lists longer
+ * than 2048 entries are split into partials (the workspace needs room for
+ * B*q_chunk*ceil(ceil(topk/64)/32) of them, else WORKSPACE_TOO_SMALL);
+ * SPLASH_FLAG_FORCE_SPLIT takes split_pages <= 32 (groups of 64 entries).
+ * SPLASH_FLAG_DEBUG_CHECK validates counts, positions and their pages.  Other
+ * arguments as for splash_mla_attend.
+ */
+int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* block_table,
+                           const int32_t* seq_lens, int32_t q_chunk, const int32_t* topk_idx,
+                           const int32_t* topk_count, int32_t topk, void* out, float* lse,
+                           const splash_mla_desc* desc, void* workspace, size_t ws_bytes,
+                           void* stream);
+
+/*
  * DOP regroup (Sec. 3 "DOP: Computation"; App. E, DOP transfer).  With
  * sharded projections, rank t of T holds all N current query rows for its
  * heads_local = H/T heads (global heads [t*H/T, (t+1)*H/T)); the owner of a

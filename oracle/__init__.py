@@ -24,8 +24,9 @@ torch dtypes).
 from . import dop
 from .formats import bf16_bits_to_f64, e4m3_bits_to_f64
 from .mla import (gather_history, mla_attention, mla_attention_sampled,
-                  merge_partials, attention_rows)
+                  merge_partials, attention_rows, gather_positions, mla_attention_topk)
 
-__all__ = ["dop", "bf16_bits_to_f64", "e4m3_bits_to_f64", "gather_history",
+__all__ = ["dop", "bf16_bits_to_f64", "e4m3_bits_to_f64", "gather_history", "gather_positions",
+           "mla_attention_topk",
            "mla_attention", "mla_attention_sampled", "merge_partials",
            "attention_rows"]

@@ -147,6 +147,41 @@ def mla_attention_sampled(q, kv, block_table, seq_lens, q_chunk, softmax_scale,
     return outs, lses
 
 
+def gather_positions(kv, kv_scales, block_table, b, positions, kv_dtype):
+    """Rows of request b's history at the given token positions, decoded to
+    float64 [len(positions), 576] (the same block-table walk as
+    gather_history, for an arbitrary list of positions)."""
+    j = np.asarray(positions, dtype=np.int64)
+    phys = block_table[b, j // PAGE].astype(np.int64) * PAGE + j % PAGE
+    rows = kv.reshape(-1, kv.shape[-1])[phys]
+    if kv_dtype == 0:
+        return bf16_bits_to_f64(rows)
+    return e4m3_bits_to_f64(rows) * kv_scales.reshape(-1).astype(np.float64)[phys][:, None]
+
+
+def mla_attention_topk(q, kv, block_table, seq_lens, q_chunk, softmax_scale, topk_idx, topk_count,
+                       kv_dtype=0, kv_scales=None):
+    """Top-k (sparse) attention: row n = b*q_chunk + i attends only the token
+    positions topk_idx[n, :topk_count[n]] of request b's history (each within
+    its causal prefix), with the same logits, values and log-sum-exp as the
+    dense definition.  Every listed position is one key (a position listed
+    twice would count twice); a row with an empty list gets out = 0, lse =
+    -inf.  Returns float64 out [B*q, H, 512] and lse [B*q, H]."""
+    H = q.shape[1]
+    sigma = _sigma(softmax_scale)
+    N = int(len(seq_lens)) * q_chunk
+    out = np.zeros((N, H, DIM_V))
+    lse = np.full((N, H), -np.inf)
+    for n in range(N):
+        b = n // q_chunk
+        c = int(topk_count[n])
+        K = gather_positions(kv, kv_scales, block_table, b, topk_idx[n, :c], kv_dtype)
+        Q = bf16_bits_to_f64(q[n:n + 1])
+        o, l = attention_rows(Q, K, sigma, np.array([c]))
+        out[n], lse[n] = o[0], l[0]
+    return out, lse
+
+
 def merge_partials(parts_out, parts_lse):
     """Merge attention over disjoint key sets into attention over their union.
 

@@ -70,6 +70,8 @@ _SIGNATURES = {
     "splash_mla_attend_units": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine_splits": (ctypes.c_int, [_I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_combine": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP]),
+    "splash_mla_attend_topk": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ,
+                                              _VP]),
     "splash_dop_pack_q": (ctypes.c_int, [_VP, _VP, _VP, _I32, _I32, _VP, _VP]),
     "splash_dop_unpack_q": (ctypes.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
     "splash_dop_pack_out": (ctypes.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
@@ -202,6 +204,15 @@ def splash_mla_attend_shard(q, kv_pages, block_table, seq_lens, q_chunk: int, ke
                                          _ptr(key_begin), _ptr(key_end), num_shards, shard, _ptr(part_out),
                                          _ptr(part_lse), ctypes.byref(desc), _ptr(workspace),
                                          workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_attend_topk(q, kv_pages, block_table, seq_lens, q_chunk: int, topk_idx, topk_count, out, lse,
+                           desc: MlaDesc, workspace, stream=None) -> None:
+    """Row n attends the positions topk_idx[n, :topk_count[n]] of its request's history."""
+    _check(lib().splash_mla_attend_topk(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
+                                        _ptr(topk_idx), _ptr(topk_count), int(topk_idx.shape[1]), _ptr(out), _ptr(lse),
+                                        ctypes.byref(desc), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def splash_dop_pack_q(q_nope, q_rope, row_order, send, stream=None) -> None:

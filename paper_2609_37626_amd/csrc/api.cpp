@@ -159,6 +159,10 @@ struct Shard {
   const int32_t* key_begin = nullptr;
   const int32_t* key_end = nullptr;
   int32_t num_shards = 0, shard = 0;
+  // the top-k variant (splash_mla_attend_topk) travels the same way
+  const int32_t* topk_idx = nullptr;
+  const int32_t* topk_count = nullptr;
+  int32_t topk = 0;
 };
 
 int check_device_data(const int32_t* block_table, const int32_t* seq_lens, int32_t q_chunk,
@@ -188,6 +192,8 @@ int do_plan(const int32_t* seq_lens, int32_t q_chunk, const splash_mla_desc* d, 
   p.seq_lens = seq_lens;
   p.key_begin = sh.key_begin;
   p.key_end = sh.key_end;
+  p.topk_count = sh.topk_count;
+  p.unit_cap = sh.topk_idx ? kTopkUnitPages : kMaxUnitPages;
   p.B = d->batch;
   p.q_chunk = q_chunk;
   p.G = G;
@@ -210,6 +216,9 @@ int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_ta
   a.seq_lens = seq_lens;
   a.key_begin = sh.key_begin;
   a.key_end = sh.key_end;
+  a.topk_idx = sh.topk_idx;
+  a.topk_count = sh.topk_count;
+  a.topk = sh.topk;
   a.out = out;
   a.lse = lse;
   a.bt_stride = d->max_pages_per_seq;
@@ -237,7 +246,8 @@ int do_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_d
   c.H = d->num_heads;
   c.out = out;
   c.out_lse = lse;
-  c.write_empty = sh.key_end != nullptr;  // a shard lists its tiles with no key, to be written empty
+  // a shard or a top-k plan lists its tiles with no key, to be written empty
+  c.write_empty = sh.key_end != nullptr || sh.topk_idx != nullptr;
   c.out_f32 = sh.key_end != nullptr;
   c.num_shards = sh.key_end ? sh.num_shards : 0;
   c.shard = sh.shard;
@@ -379,6 +389,52 @@ int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_
     if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   if ((st = do_plan(seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
+}
+
+int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* block_table,
+                           const int32_t* seq_lens, int32_t q_chunk, const int32_t* topk_idx,
+                           const int32_t* topk_count, int32_t topk, void* out, float* lse,
+                           const splash_mla_desc* desc, void* workspace, size_t ws_bytes, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->batch == 0) return SPLASH_OK;
+  if (!topk_idx || !topk_count) return fail(SPLASH_ERR_INVALID_ARGUMENT, "topk_idx and topk_count must be non-NULL");
+  if (topk < 1 || topk > (1 << 24)) return fail(SPLASH_ERR_INVALID_ARGUMENT, "topk must be in [1, 2^24] (got %d)", topk);
+  if ((desc->flags & SPLASH_FLAG_FORCE_SPLIT) && desc->split_pages > kTopkUnitPages)
+    return fail(SPLASH_ERR_UNSUPPORTED, "a top-k unit holds at most %d x 64 entries", kTopkUnitPages);
+  if ((st = check_tensors(q, kv_pages, block_table, out, lse)) != SPLASH_OK) return st;
+  Workspace wv;
+  if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
+  const int64_t N = (int64_t)desc->batch * q_chunk;
+  const int64_t groups = ceil_div(topk, kPage);
+  const int64_t need = groups > kTopkUnitPages ? N * ceil_div((int32_t)groups, kTopkUnitPages) : 0;
+  if (wv.max_partials < need)
+    return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL, "lists longer than %d entries are split: need %lld partial slots, have %d",
+                kTopkUnitPages * kPage, (long long)need, wv.max_partials);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (desc->flags & SPLASH_FLAG_DEBUG_CHECK) {
+    int32_t* res = wv.header + kHdrDebug;
+    hipError_t e = launch_topk_check(block_table, seq_lens, topk_idx, topk_count, (int32_t)N, q_chunk, topk,
+                                     desc->max_pages_per_seq, desc->num_pages, res, s);
+    if (e != hipSuccess) return hip_fail(e, "check launch");
+    int32_t host = 0;
+    e = hipMemcpyAsync(&host, res, sizeof host, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "check readback");
+    if (host != INT32_MAX)
+      return fail(SPLASH_ERR_INVALID_ARGUMENT,
+                  "row %d: count outside [0, topk], a position outside the row's visible prefix, or its block-table "
+                  "entry outside [0, num_pages)",
+                  host - 1);
+  }
+  Shard sh;
+  sh.topk_idx = topk_idx;
+  sh.topk_count = topk_count;
+  sh.topk = topk;
+  if ((st = do_plan(seq_lens, q_chunk, desc, wv, s, sh)) != SPLASH_OK) return st;
+  if ((st = do_attend_units(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s, sh)) != SPLASH_OK)
+    return st;
+  return do_combine_splits(q_chunk, out, lse, desc, wv, s, sh);
 }
 
 int splash_mla_attend_shard(const void* q, const void* kv_pages, const int32_t* block_table,

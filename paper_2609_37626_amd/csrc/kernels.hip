@@ -91,9 +91,12 @@ __device__ __forceinline__ float wave_xor32(float v) { return __shfl_xor(v, 32, 
 // ============================================================== planner ===
 
 // Pages of tile t: its whole causal prefix, or under a shard its keys in
-// [key_begin[b], min(prefix, key_end[b])) (key_begin a page boundary).
+// [key_begin[b], min(prefix, key_end[b])) (key_begin a page boundary), or
+// for the top-k variant its list entries in groups of 64.
 __device__ __forceinline__ int32_t dev_tile_pages(const int32_t* seq_lens, int32_t q_chunk, int32_t t,
-                                                  const int32_t* key_begin, const int32_t* key_end) {
+                                                  const int32_t* key_begin, const int32_t* key_end,
+                                                  const int32_t* topk_count) {
+  if (topk_count) return ceil_div(topk_count[t], kPage);
   int32_t b = t / q_chunk, i = t - b * q_chunk;
   int32_t L = tile_keys(seq_lens[b], q_chunk, i);
   if (key_end) {
@@ -197,16 +200,19 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   // (the combine turns each tile's parts into its fp32 result), and tiles
   // with no key in the shard are listed for the combine with no parts.
   const bool shard = p.key_end != nullptr;
+  // tiles with no key (a shard's, or a top-k row with an empty list) are
+  // listed for the combine with no parts, which writes out = 0, lse = -inf
+  const bool list_empty = shard || p.topk_count != nullptr;
   int32_t* hdr = p.ws.header;
   auto pages_of = [&](int32_t t) -> int32_t {
-    return cached ? s_pages[t] : dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end);
+    return cached ? s_pages[t] : dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end, p.topk_count);
   };
 
   // 1. page counts (cached), total and largest tile.
   int64_t tot = 0;
   int32_t mx = 0;
   for (int32_t t = tid; t < T; t += 1024) {
-    const int32_t P = dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end);
+    const int32_t P = dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end, p.topk_count);
     if (cached) s_pages[t] = P;
     tot += P;
     mx = P > mx ? P : mx;
@@ -249,10 +255,10 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       const int k = 64 * r + lane;
       int32_t ck = 0;
       if (k < kNumCandidates) {
-        ck = plan_candidate_size(s_parts[k], max_pages);
-        if (k > 0 && plan_candidate_size(s_parts[k - 1], max_pages) == ck) ck = 0;
+        ck = plan_candidate_size(s_parts[k], max_pages, p.unit_cap);
+        if (k > 0 && plan_candidate_size(s_parts[k - 1], max_pages, p.unit_cap) == ck) ck = 0;
       } else if (k == kNumCandidates && p.forced_chunk > 0) {
-        ck = p.forced_chunk < kMaxUnitPages ? p.forced_chunk : kMaxUnitPages;
+        ck = p.forced_chunk < p.unit_cap ? p.forced_chunk : p.unit_cap;
       }
       if (k <= kNumCandidates) s_cand[k] = ck;
       const uint64_t keep = __builtin_amdgcn_ballot_w64(ck > 0);
@@ -288,7 +294,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
 #pragma unroll 4
         for (int32_t t = slice; t < T; t += nsl) count(s_pages[t]);
       } else {
-        for (int32_t t = slice; t < T; t += nsl) count(dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end));
+        for (int32_t t = slice; t < T; t += nsl) count(dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end, p.topk_count));
       }
       s_w[slice][j] = W;
       s_s[slice][j] = S;
@@ -333,7 +339,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   // + U + U [q_{G-1-j} > 0] independent of C, so a running max of v over j
   // and a binary search for nl(C) = #{r : q_r > C} price a cap in O(log G).
   bool fold = p.forced_chunk == 0 && !shard &&
-              fold_applicable(T, p.G, kMaxWorkers, max_pages, total_pages, s_best, kPlanCosts);  // uniform
+              fold_applicable(T, p.G, kMaxWorkers, max_pages, total_pages, s_best, kPlanCosts, p.unit_cap);
   int32_t cap = 0, nl = 0;
   if (fold) {
     // counting sort of the tiles by pages, longest first: the histogram, the
@@ -416,7 +422,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     const int32_t P = t < T ? pages_of(t) : 0;
     int32_t n = 0, sp = 0;
     if (t < T) tile_units(t, P, &n, &sp);
-    const int32_t f = (sp > 0 || (shard && t < T && P == 0)) ? 1 : 0;
+    const int32_t f = (sp > 0 || (list_empty && t < T && P == 0)) ? 1 : 0;
     int32_t tu, ts, tf;
     const int32_t eu = block_exclusive_scan(n, s_scan, &tu) + carry_u;
     const int32_t es = block_exclusive_scan(sp, s_scan, &ts) + carry_s;
@@ -582,6 +588,26 @@ __device__ __forceinline__ void dma_b128(const void* sbase, uint32_t voff, const
       : "v"(voff), "s"(sbase), "s"(m0)
       : "memory");
 }
+// The same loads from a per-lane 64-bit address (gathered rows anywhere in
+// the pool).
+__device__ __forceinline__ void dma_b128_v(uint64_t vaddr, const uint8_t LDS_AS* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(vaddr), "s"(m0)
+      : "memory");
+}
+__device__ __forceinline__ void dma_b32_v(uint64_t vaddr, const uint8_t LDS_AS* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(vaddr), "s"(m0)
+      : "memory");
+}
 __device__ __forceinline__ void dma_b32(const void* sbase, uint32_t voff, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
@@ -613,6 +639,28 @@ __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, 
       asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_and_b32 %0, 31, %0\n\tv_lshlrev_b32 %0, 2, %0" : "=v"(voff));
       dma_b32(step_scales, voff, buf + 18432);
     }
+  }
+}
+
+// Top-k variant: the lane's row of the step is a gathered pool row, at
+// row_addr (its chunk included); its token scale (fp8, waves 2 and 3) at
+// scale_addr.  Same LDS placement as issue_one.
+template <bool FP8, int t>
+__device__ __forceinline__ void issue_one_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave) {
+  if constexpr (!FP8) {
+    dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 1024 * wave);
+  } else {
+    if (t < 4 || wave + 4 * t < 18)
+      dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+    else
+      dma_b32_v(scale_addr, buf + 18432);
+  }
+}
+template <bool FP8, int t = 0>
+__device__ __forceinline__ void issue_from_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave) {
+  if constexpr (t < StepLayout<FP8>::kLoadsPerStep) {
+    issue_one_v<FP8, t>(row_addr, scale_addr, buf, wave);
+    issue_from_v<FP8, t + 1>(row_addr, scale_addr, buf, wave);
   }
 }
 
@@ -719,14 +767,19 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
   }
 }
 
-template <bool FP8>
+// TOPK: the top-k variant.  Row n attends the first topk_count[n] token
+// positions of its list topk_idx[n] (of request b = n / q_chunk); a unit
+// covers list entries [64 p0, 64 p1) instead of pages, and its prologue
+// resolves every entry to its pool row (into the LDS the block-table slice
+// uses otherwise), from which each lane loads its staged row.
+template <bool FP8, bool TOPK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   using L = StepLayout<FP8>;
   constexpr int kPOff = L::kRing;                    // P exchange area, two steps
   constexpr int kLOff = kPOff + 2 * kPBytes;         // per-head normaliser, 128 floats
-  constexpr int kBtOff = kLOff + kMaxHeads * 4;      // block-table slice
-  constexpr int kSmem = kBtOff + kMaxUnitPages * 4;
+  constexpr int kBtOff = kLOff + kMaxHeads * 4;      // block-table slice (top-k: the unit's pool rows)
+  constexpr int kSmem = kBtOff + (TOPK ? kTopkUnitPages * kPage : kMaxUnitPages) * 4;
   static_assert(kSmem <= 163840 - 64, "LDS budget");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
   __shared__ int4 s_unit;
@@ -823,12 +876,28 @@ void attend_kernel(AttendLaunch a) {
       p1 += first;
       Lk = min(Lk, a.key_end[b]);
     }
+    if constexpr (TOPK) Lk = a.topk_count[tile];  // entries of the row's list
     const int key_begin = p0 * kPage;
     const int key_end = min(p1 * kPage, Lk);
     const int nsteps = (key_end - key_begin + kStepKeys - 1) / kStepKeys;
 
-    const int32_t* bt = a.block_table + (size_t)b * a.bt_stride + p0;
-    for (int k = tid; k < p1 - p0; k += 256) s_bt[k] = bt[k];
+    if constexpr (TOPK) {
+      // pool row of every list entry of the unit (entries past the list end
+      // read pool row 0, whose keys the tail mask removes)
+      const int32_t* sel = a.topk_idx + (size_t)tile * a.topk;
+      const int32_t* btr = a.block_table + (size_t)b * a.bt_stride;
+      for (int e = tid; e < (p1 - p0) * kPage; e += 256) {
+        int row = 0;
+        if (key_begin + e < key_end) {
+          const int pos = sel[key_begin + e];
+          row = btr[pos >> 6] * kPage + (pos & (kPage - 1));
+        }
+        s_bt[e] = row;
+      }
+    } else {
+      const int32_t* bt = a.block_table + (size_t)b * a.bt_stride + p0;
+      for (int k = tid; k < p1 - p0; k += 256) s_bt[k] = bt[k];
+    }
 
     // Query fragments: B operands, k = dims 16ks + 8h + [0, 8), row = head
     bf16x8 qf[36];
@@ -855,6 +924,14 @@ void attend_kernel(AttendLaunch a) {
     auto step_phys = [&](int j) {
       return __builtin_amdgcn_readfirstlane(s_bt[((key_begin + j * kStepKeys) >> 6) - p0]);
     };
+    // top-k: pool row of the lane's staged row of step j, and (fp8) of the
+    // token scale it loads; their addresses
+    auto lane_row = [&](int j) { return s_bt[j * kStepKeys + dma_row]; };
+    auto scale_row = [&](int j) { return FP8 ? s_bt[j * kStepKeys + (lane & 31)] : 0; };
+    auto row_addr = [&](int r) {
+      return (uint64_t)(uintptr_t)kv + (uint64_t)(uint32_t)r * L::kRowBytes + (src_lane - dma_row * L::kRowBytes);
+    };
+    auto scale_addr = [&](int r) { return (uint64_t)(uintptr_t)a.kv_scales + (uint64_t)(uint32_t)r * 4; };
     // ring slot of step j; the offset is laundered so the compiler keeps one
     // scalar per step instead of deriving per-lane induction variables
     auto slot_buf = [&](int j) {
@@ -877,8 +954,12 @@ void attend_kernel(AttendLaunch a) {
 #pragma unroll
       for (int j = 0; j < L::kDist; ++j)
         if (j < nsteps) {
-          const int ph = step_phys(j);
-          issue_step<FP8>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
+          if constexpr (TOPK) {
+            issue_from_v<FP8>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave);
+          } else {
+            const int ph = step_phys(j);
+            issue_step<FP8>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
+          }
         }
 
 #pragma unroll
@@ -892,8 +973,13 @@ void attend_kernel(AttendLaunch a) {
 
       // page of the step staged next: read from LDS one iteration early, made
       // uniform only where the loads are issued
-      int next_phys = L::kDist < nsteps ? step_phys(L::kDist) : 0;
+      int next_phys = !TOPK && L::kDist < nsteps ? step_phys(L::kDist) : 0;
       int next_phys_v = 0;
+      // top-k: the rows of the step staged next (per lane), read one
+      // iteration early like the page above
+      int next_row = TOPK && L::kDist < nsteps ? lane_row(L::kDist) : 0;
+      int next_srow = TOPK && L::kDist < nsteps ? scale_row(L::kDist) : 0;
+      int next_row_v = 0, next_srow_v = 0;
       // One pipeline iteration: staging wait, QK of step j (interleaved with
       // half of PV of step j-1 and the loads of step j + kDist), then the
       // softmax of step j interleaved with the other half of PV of step j-1.
@@ -905,9 +991,14 @@ void attend_kernel(AttendLaunch a) {
         const int key0 = key_begin + j * kStepKeys;
         const int valid = key_end - key0;  // >= 1
         const bool pf_next = j + L::kDist < nsteps;
-        const int pf_phys = j == 0 ? next_phys : __builtin_amdgcn_readfirstlane(next_phys_v);
+        const int pf_phys = TOPK ? 0 : j == 0 ? next_phys : __builtin_amdgcn_readfirstlane(next_phys_v);
         const uint8_t* pf_src = step_src(j + L::kDist, pf_phys);
         const float* pf_scales = step_scales(j + L::kDist, pf_phys);
+        uint64_t pf_row = 0, pf_srow = 0;
+        if constexpr (TOPK) {
+          pf_row = row_addr(j == 0 ? next_row : next_row_v);
+          pf_srow = scale_addr(j == 0 ? next_srow : next_srow_v);
+        }
         uint8_t LDS_AS* pf_buf = slot_buf(j + L::kDist);
         if (L::kDist == 2 && j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
         else wait_vmcnt<0>();
@@ -974,16 +1065,30 @@ void attend_kernel(AttendLaunch a) {
             }
             // the loads of step j + kDist, spread over the stream
             if ((i & 3) == 1 && (i >> 2) < L::kLoadsPerStep && pf_next) {
-              switch (i >> 2) {
-                case 0: issue_one<FP8, 0>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 1: issue_one<FP8, 1>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 2: issue_one<FP8, 2>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 3: issue_one<FP8, 3>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 4: issue_one<FP8, 4>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 5: issue_one<FP8, 5>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 6: issue_one<FP8, 6>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                case 7: issue_one<FP8, 7>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                default: issue_one<FP8, 8>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+              if constexpr (TOPK) {
+                switch (i >> 2) {
+                  case 0: issue_one_v<FP8, 0>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 1: issue_one_v<FP8, 1>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 2: issue_one_v<FP8, 2>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 3: issue_one_v<FP8, 3>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 4: issue_one_v<FP8, 4>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 5: issue_one_v<FP8, 5>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 6: issue_one_v<FP8, 6>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 7: issue_one_v<FP8, 7>(pf_row, pf_srow, pf_buf, wave); break;
+                  default: issue_one_v<FP8, 8>(pf_row, pf_srow, pf_buf, wave); break;
+                }
+              } else {
+                switch (i >> 2) {
+                  case 0: issue_one<FP8, 0>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 1: issue_one<FP8, 1>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 2: issue_one<FP8, 2>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 3: issue_one<FP8, 3>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 4: issue_one<FP8, 4>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 5: issue_one<FP8, 5>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 6: issue_one<FP8, 6>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 7: issue_one<FP8, 7>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  default: issue_one<FP8, 8>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                }
               }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -1019,7 +1124,12 @@ void attend_kernel(AttendLaunch a) {
           }
         }
         // page of the step the next iteration stages (read now, used there)
-        next_phys_v = j + L::kDist + 1 < nsteps ? s_bt[((key_begin + (j + L::kDist + 1) * kStepKeys) >> 6) - p0] : 0;
+        if constexpr (TOPK) {
+          next_row_v = j + L::kDist + 1 < nsteps ? lane_row(j + L::kDist + 1) : 0;
+          next_srow_v = j + L::kDist + 1 < nsteps ? scale_row(j + L::kDist + 1) : 0;
+        } else {
+          next_phys_v = j + L::kDist + 1 < nsteps ? s_bt[((key_begin + (j + L::kDist + 1) * kStepKeys) >> 6) - p0] : 0;
+        }
 
         // ---- scores: token scales (fp8), the history-end mask and, on the
         // unit's first step, the reference.  Softmax in base 2; lane = one
@@ -1477,6 +1587,33 @@ __global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int
 
 __global__ void init_check(int32_t* result) { *result = INT32_MAX; }
 
+// Top-k variant: every row's count in [0, topk], every used position in the
+// row's visible prefix [0, s_b - q_chunk + i], and its page's block-table
+// entry in [0, num_pages).  Writes the smallest failing row + 1 (or 0).
+__global__ __launch_bounds__(256) void topk_check_kernel(const int32_t* bt, const int32_t* seq_lens,
+                                                         const int32_t* idx, const int32_t* count, int32_t N,
+                                                         int32_t q_chunk, int32_t topk, int32_t bt_stride,
+                                                         int32_t num_pages, int32_t* result) {
+  for (int n = blockIdx.x; n < N; n += gridDim.x) {
+    const int b = n / q_chunk, i = n - b * q_chunk;
+    const int s = seq_lens[b], c = count[n];
+    const int vis = s - q_chunk + i + 1;
+    bool bad = s < q_chunk || (int64_t)(s + kPage - 1) / kPage > bt_stride || c < 0 || c > topk;
+    if (!bad) {
+      for (int e = threadIdx.x; e < c; e += blockDim.x) {
+        const int pos = idx[(size_t)n * topk + e];
+        if (pos < 0 || pos >= vis) {
+          bad = true;
+        } else {
+          const int pg = bt[(size_t)b * bt_stride + (pos >> 6)];
+          if (pg < 0 || pg >= num_pages) bad = true;
+        }
+      }
+    }
+    if (bad) atomicMin(result, n + 1);
+  }
+}
+
 // ============================================================ launchers ===
 
 hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
@@ -1485,10 +1622,19 @@ hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
 }
 
 hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) {
-  if (a.kv_dtype == 1)
-    hipLaunchKernelGGL(attend_kernel<true>, dim3(workers), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(attend_kernel<false>, dim3(workers), dim3(256), 0, s, a);
+  if (a.kv_dtype == 1) {
+    if (a.topk_idx) {
+      hipLaunchKernelGGL((attend_kernel<true, true>), dim3(workers), dim3(256), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((attend_kernel<true, false>), dim3(workers), dim3(256), 0, s, a);
+    }
+  } else {
+    if (a.topk_idx) {
+      hipLaunchKernelGGL((attend_kernel<false, true>), dim3(workers), dim3(256), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((attend_kernel<false, false>), dim3(workers), dim3(256), 0, s, a);
+    }
+  }
   return hipGetLastError();
 }
 
@@ -1505,6 +1651,16 @@ hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_l
                          int32_t row_bytes, void* dense, hipStream_t s) {
   hipLaunchKernelGGL(gather_kernel, dim3(B), dim3(256), 0, s, (const uint8_t*)kv, bt, seq_lens, B, bt_stride,
                      row_bytes, (uint8_t*)dense);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* idx, const int32_t* count,
+                             int32_t N, int32_t q_chunk, int32_t topk, int32_t bt_stride, int32_t num_pages,
+                             int32_t* result, hipStream_t s) {
+  hipLaunchKernelGGL(init_check, dim3(1), dim3(1), 0, s, result);
+  int blocks = N < 1024 ? N : 1024;
+  hipLaunchKernelGGL(topk_check_kernel, dim3(blocks), dim3(256), 0, s, bt, seq_lens, idx, count, N, q_chunk, topk,
+                     bt_stride, num_pages, result);
   return hipGetLastError();
 }
 

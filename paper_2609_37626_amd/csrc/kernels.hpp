@@ -40,7 +40,9 @@ struct PlanLaunch {
   const int32_t* seq_lens;
   const int32_t* key_begin;  // shard: request b's keys [key_begin[b], key_end[b]) (nullptr: whole history)
   const int32_t* key_end;
+  const int32_t* topk_count;  // top-k variant: row n attends its first topk_count[n] selected tokens
   int32_t B, q_chunk, G, forced_chunk;
+  int32_t unit_cap;           // largest unit in pages (kMaxUnitPages, or kTopkUnitPages for top-k)
   Workspace ws;
 };
 
@@ -52,6 +54,9 @@ struct AttendLaunch {
   const int32_t* seq_lens;
   const int32_t* key_begin;  // shard (see PlanLaunch): unit pages count from key_begin[b] / 64
   const int32_t* key_end;
+  const int32_t* topk_idx;    // top-k variant: [N, topk] selected token positions of each row
+  const int32_t* topk_count;  // [N] how many of them are used
+  int32_t topk;
   void* out;
   float* lse;
   int32_t bt_stride, q_chunk, H, kv_dtype, B;
@@ -81,6 +86,9 @@ hipError_t launch_attend(const AttendLaunch& p, int32_t workers, hipStream_t s);
 hipError_t launch_combine(const CombineLaunch& p, hipStream_t s);
 hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_lens, int32_t B,
                          int32_t bt_stride, int32_t row_bytes, void* dense, hipStream_t s);
+hipError_t launch_topk_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* idx, const int32_t* count,
+                             int32_t N, int32_t q_chunk, int32_t topk, int32_t bt_stride, int32_t num_pages,
+                             int32_t* result, hipStream_t s);
 hipError_t launch_dop_pack_q(const void* q_nope, const void* q_rope, const int32_t* order, int32_t n, int32_t hl,
                              void* send, hipStream_t s);
 hipError_t launch_dop_unpack_q(const void* recv, int32_t T, int32_t n, int32_t hl, void* q_owner, hipStream_t s);

@@ -20,6 +20,7 @@ constexpr int kDimV = 512;         // d_z = d_c
 constexpr int kMaxHeads = 128;
 constexpr int kStepKeys = 32;      // keys per pipeline step (half a page)
 constexpr int kMaxUnitPages = 1024;  // the block-table slice of one unit is staged in LDS
+constexpr int kTopkUnitPages = 32;   // top-k variant: a unit holds 32 x 64 selected rows' addresses in LDS
 constexpr int kMaxWorkers = 1024;    // the fold plan's per-worker table is sized for this many
 constexpr int kHeaderInts = 1152;    // 64 header slots, then the per-worker table (kMaxWorkers + 1)
 constexpr int kPlanLdsTiles = 8192;  // planner: tile data cached in LDS, and the unit queue ordered longest
@@ -98,9 +99,11 @@ SPLASH_HD int32_t plan_candidate_parts(int32_t k) {
   }
   return parts;
 }
-SPLASH_HD int32_t plan_candidate_size(int32_t parts, int32_t max_pages) {
+// (cap: the largest unit, kMaxUnitPages, or smaller for the top-k variant,
+// whose unit holds its selected rows' addresses in the same LDS)
+SPLASH_HD int32_t plan_candidate_size(int32_t parts, int32_t max_pages, int32_t cap = kMaxUnitPages) {
   int32_t c = ceil_div(max_pages, parts);
-  if (c > kMaxUnitPages) c = kMaxUnitPages;
+  if (c > cap) c = cap;
   return c < 1 ? 1 : c;
 }
 SPLASH_HD int32_t plan_candidate(int32_t k, int32_t max_pages) {
@@ -173,8 +176,8 @@ SPLASH_HD int64_t fold_cost(int32_t C, const Q& q, int32_t G, int32_t max_partia
 // two, so the busiest worker runs at least half of it (and at least the
 // mean), a lower bound on every fold's estimate.
 SPLASH_HD bool fold_applicable(int32_t T, int32_t G, int32_t max_workers, int32_t max_pages, int64_t total_pages,
-                               int64_t best_cost, PlanCosts k) {
-  if (!(T >= 1 && T <= G && G <= max_workers && max_pages >= 2 && max_pages <= kMaxUnitPages)) return false;
+                               int64_t best_cost, PlanCosts k, int32_t cap = kMaxUnitPages) {
+  if (!(T >= 1 && T <= G && G <= max_workers && max_pages >= 2 && max_pages <= cap)) return false;
   int64_t busy = 8 * (int64_t)max_pages + k.unit_x16;
   const int64_t mean = 16 * total_pages / G;
   if (mean > busy) busy = mean;

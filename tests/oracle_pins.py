@@ -286,3 +286,54 @@ def pin_fp8_dequant(seed=8):
             qt, kt, vt, attn_mask=mask, scale=float(batch.softmax_scale))[0].permute(1, 0, 2).numpy()
         worst = max(worst, np.abs(out[b * 2:(b + 1) * 2] - ref).max())
     return worst
+
+
+def topk_lists(lens, q_chunk, rng, frac=0.4):
+    """Distinct visible positions for every row (a random subset, shuffled),
+    padded with -1 to a common length; returns idx [N, k] and count [N]."""
+    rows = []
+    for b, s in enumerate(lens):
+        for i in range(q_chunk):
+            vis = int(s) - q_chunk + i + 1
+            c = max(1, int(round(frac * vis)))
+            rows.append(rng.permutation(vis)[:c])
+    k = max(len(r) for r in rows)
+    idx = np.full((len(rows), k), -1, dtype=np.int32)
+    for n, r in enumerate(rows):
+        idx[n, :len(r)] = r
+    return idx, np.array([len(r) for r in rows], dtype=np.int32)
+
+
+def pin_topk_sdpa(seed=11, B=3, H=4, q_chunk=3, s_max=300):
+    """Top-k rows against torch's float64 scaled-dot-product attention on the
+    dense histories with a mask that keeps exactly each row's listed
+    positions."""
+    dense, q_bits, pool, table, lens = random_dense_case(seed, B, H, q_chunk, s_max)
+    rng = np.random.Generator(np.random.PCG64(seed + 1))
+    idx, cnt = topk_lists(lens, q_chunk, rng)
+    out, lse = oracle.mla_attention_topk(q_bits, pool, table, lens, q_chunk, W.SOFTMAX_SCALE, idx, cnt)
+    worst = 0.0
+    for b, keys_bits in enumerate(dense):
+        s = keys_bits.shape[0]
+        k = torch.from_numpy((keys_bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+        for i in range(q_chunk):
+            n = b * q_chunk + i
+            qt = torch.from_numpy((q_bits[n].astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+            mask = torch.zeros(s, dtype=torch.bool)
+            mask[torch.from_numpy(idx[n, :cnt[n]].astype(np.int64))] = True
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                qt.unsqueeze(1), k.unsqueeze(0).expand(H, s, 576), k[:, :512].unsqueeze(0).expand(H, s, 512),
+                attn_mask=mask.unsqueeze(0).unsqueeze(0).expand(H, 1, s), scale=float(W.SOFTMAX_SCALE))
+            worst = max(worst, np.abs(out[n] - ref[:, 0].numpy()).max())
+    return worst
+
+
+def pin_topk_all_positions(seed=12, B=2, H=2, q_chunk=2, s_max=120):
+    """Listing every visible position (in shuffled order) is dense attention:
+    equal to the pure-Python brute force."""
+    dense, q_bits, pool, table, lens = random_dense_case(seed, B, H, q_chunk, s_max)
+    rng = np.random.Generator(np.random.PCG64(seed + 1))
+    idx, cnt = topk_lists(lens, q_chunk, rng, frac=1.0)
+    out, lse = oracle.mla_attention_topk(q_bits, pool, table, lens, q_chunk, W.SOFTMAX_SCALE, idx, cnt)
+    ref_out, ref_lse = brute_force(dense, q_bits, q_chunk, float(W.SOFTMAX_SCALE))
+    return max(np.abs(out - ref_out).max(), np.abs(lse - ref_lse).max())

@@ -332,3 +332,20 @@ def test_dop_head_order_worked_example():
     q1 = dop.unpack_q(recv[1], 2, 2)
     assert q1[0, 3, 0] == 30 and q1[1, 2, 5] == 200 + 20 + 5   # row 0 head 3; row 2 head 2, dim 5
     assert np.array_equal(q1[1, 3], q[2, 3]) and np.array_equal(q1[0, 0], q[0, 0])
+
+
+# ------------------------------------------------------------------ top-k ---
+
+def test_topk_matches_masked_sdpa():
+    assert pins.pin_topk_sdpa() < 1e-12
+
+
+def test_topk_of_every_position_is_dense_attention():
+    assert pins.pin_topk_all_positions() < 1e-12
+
+
+def test_topk_empty_list_is_empty():
+    dense, q_bits, pool, table, lens = pins.random_dense_case(13, 2, 2, 1)
+    idx = np.full((2, 4), -1, dtype=np.int32)
+    out, lse = oracle.mla_attention_topk(q_bits, pool, table, lens, 1, 0.07, idx, np.array([0, 0], np.int32))
+    assert np.all(out == 0.0) and np.all(np.isneginf(lse))
