@@ -20,6 +20,13 @@
  *   lse[n,h]   = ln sum_j exp(z_j)                (natural log, scaled logits)
  *   out[n,h,:] = sum_j exp(z_j - lse[n,h]) * K_j[0:512]
  *
+ * Entry points: the whole step (splash_mla_attend), its phases (plan,
+ * attend_units, combine_splits, run), the standalone LSE merge
+ * (splash_mla_combine), and around the same core: one position shard of the
+ * histories (splash_mla_attend_shard), attention over listed positions only
+ * (splash_mla_attend_topk), and the DOP regroup of query and output rows
+ * (splash_dop_*).
+ *
  * Conventions for every entry point:
  *  - All tensor pointers are DEVICE pointers owned by the caller; the library
  *    never allocates or frees device memory in these calls and keeps no

@@ -1,5 +1,6 @@
-// gfx950 kernels of libsplash_attn: split planner, paged MLA attend, LSE
-// combine, page gather and device-data check.
+// gfx950 kernels of libsplash_attn: split planner, paged MLA attend (whole
+// histories, position shards, or listed top-k positions), LSE combine, page
+// gather and device-data checks.  (The DOP regroup kernels are in dop.hip.)
 //
 // Attend kernel design (one persistent workgroup per compute unit):
 //  * Work unit = (query row n with all H heads, page range).  Under a fold
