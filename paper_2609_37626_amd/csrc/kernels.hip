@@ -732,6 +732,34 @@ __device__ __forceinline__ bf16x8 load_v_frag(const uint8_t LDS_AS* buf, const u
   }
 }
 
+// Operand fragments as the LDS reads return them (fp8: the 8 codes) and
+// their conversion to the MFMA's bf16.  The stream converts a fragment in
+// the slot that uses it, so the read has the slots since its issue to land;
+// converting right at the read would wait for it there.
+template <bool FP8>
+using FragRaw = typename std::conditional<FP8, u32x2, bf16x8>::type;
+template <bool FP8>
+__device__ __forceinline__ FragRaw<FP8> load_k_raw(const uint8_t LDS_AS* buf, const uint32_t* kbase, int ks) {
+  if constexpr (!FP8) return *(const bf16x8 LDS_AS*)(buf + kbase[ks & 3] + 4096 * (ks >> 2));
+  else return *(const u32x2 LDS_AS*)(buf + kbase[ks & 3] + 2048 * (ks >> 2));
+}
+template <bool FP8>
+__device__ __forceinline__ FragRaw<FP8> load_v_raw(const uint8_t LDS_AS* buf, const uint32_t (*vbase)[2], int cb,
+                                                   int kh) {
+  if constexpr (!FP8) {
+    return load_v_frag<false>(buf, vbase, cb, kh);
+  } else {
+    const i32x2 raw = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+        (i32x2 LDS_AS*)(buf + vbase[cb & 1][0] + 2048 * (cb >> 1) + 1024 * kh));
+    return __builtin_bit_cast(u32x2, raw);
+  }
+}
+template <bool FP8>
+__device__ __forceinline__ bf16x8 frag_bf16(const FragRaw<FP8>& r) {
+  if constexpr (FP8) return fp8x8_to_bf16(r);
+  else return r;
+}
+
 // P^T operand fragment (head block hb, key half kh) from the P exchange area:
 // head hh's 32 weights are 64 B, slot (kh, half) at ((2kh + half) ^ (hh>>2 & 3)) * 16.
 __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t half) {
@@ -1028,17 +1056,20 @@ void attend_kernel(AttendLaunch a) {
         // 32 - kPV1 PV MFMAs run under the softmax (stream 2).
         constexpr int kPV1 = 8;
         f32x16 sacc;
-        bf16x8 pf[4], pf1[4], vf[3];
+        bf16x8 pf[4], pf1[4];
+        FragRaw<FP8> vf[3];  // V fragments of three column blocks, as read
+        bf16x8 vcur;         // that of the current column block, converted
         {
           constexpr int kKPre = 4;  // K fragments in flight
-          bf16x8 kf[kKPre];
+          FragRaw<FP8> kf[kKPre];
+          bf16x8 ka_prev;  // fp8: the converted fragment the previous QK MFMA was issued with
 #pragma unroll
-          for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_frag<FP8>(buf, kbase, ks);
+          for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_raw<FP8>(buf, kbase, ks);
           if constexpr (kPV) {
 #pragma unroll
             for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 0, h));
-            vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
-            vf[1] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + 1, 0);
+            vf[0] = load_v_raw<FP8>(vbuf, vbase, 4 * wave, 0);
+            vf[1] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + 1, 0);
           }
 #pragma unroll
           for (int i = 0; i < 36; ++i) {
@@ -1050,16 +1081,24 @@ void attend_kernel(AttendLaunch a) {
               // V fragment two column blocks ahead (c = 4kh + cbl); its ring
               // entry last served column block c - 1
               const int cn = (q >> 2) + 2;
-              vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+              vf[cn % 3] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
-            const bf16x8 ka = kf[i % kKPre];
-            if (i + kKPre < 36) kf[i % kKPre] = load_k_frag<FP8>(buf, kbase, i + kKPre);
+            const bf16x8 ka = frag_bf16<FP8>(kf[i % kKPre]);
+            if constexpr (FP8) {
+              // the conversion must not reuse the registers of the MFMA just
+              // issued (the asm hides that read from the compiler): keeping
+              // that fragment live through it gives this one its own
+              if (i > 0) asm volatile("" ::"v"(ka), "v"(ka_prev));
+              ka_prev = ka;
+            }
+            if (i + kKPre < 36) kf[i % kKPre] = load_k_raw<FP8>(buf, kbase, i + kKPre);
             if (i == 0) mfma_qk<true, FP8>(sacc, ka, qf[i]);
             else mfma_qk<false, FP8>(sacc, ka, qf[i]);
             if (q != kNone) {
               const int c = q >> 2, hb = q & 3;
               const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
-              o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+              if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
+              o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
               // key half 1 P fragment of this head block, in the registers
               // of the half 0 one, which column block 3 has just read last
               if (c == 3) pf1[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
@@ -1102,10 +1141,11 @@ void attend_kernel(AttendLaunch a) {
             const int c = q >> 2, hb = q & 3;
             if (hb == 0 && c + 2 < 8) {
               const int cn = c + 2;
-              vf[cn % 3] = load_v_frag<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
+              vf[cn % 3] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
             const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
-            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c % 3], pv, o[c & 3][hb], 0, 0, 0);
+            if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
+            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
             // (as in stream 1) the key half 1 P fragment after the last read
             // of the half 0 one
             if (c == 3) pf1[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
