@@ -22,11 +22,11 @@ hand-worked example, and the format definitions cross-checked with numpy and
 torch dtypes).
 """
 from . import dop
-from .formats import bf16_bits_to_f64, e4m3_bits_to_f64
+from .formats import DS_ROW_BYTES, bf16_bits_to_f64, ds_rows_to_f64, e4m3_bits_to_f64
 from .mla import (gather_history, mla_attention, mla_attention_sampled,
                   merge_partials, attention_rows, gather_positions, mla_attention_topk)
 
-__all__ = ["dop", "bf16_bits_to_f64", "e4m3_bits_to_f64", "gather_history", "gather_positions",
+__all__ = ["dop", "bf16_bits_to_f64", "e4m3_bits_to_f64", "ds_rows_to_f64", "DS_ROW_BYTES", "gather_history", "gather_positions",
            "mla_attention_topk",
            "mla_attention", "mla_attention_sampled", "merge_partials",
            "attention_rows"]

@@ -1,4 +1,4 @@
-"""Decoders of the two cache formats, written from their definitions.
+"""Decoders of the cache formats, written from their definitions.
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
@@ -10,7 +10,21 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
   infinities and the largest finite magnitude is 448.  The B200 runs keep the
   KV cache in FP8 E4M3 (App. C).
 
-Both decoders are exact in float64.
+* Latent-row format (the DeepSeek-V3.2 cache row of App. B, "Theoretical
+  Scenarios for DCU and H200", residency assumptions: FP8 latent with its
+  scales and BF16 RoPE; the indexer state that completes the paper's 788
+  bytes per token and layer is a separate pool that attention never reads).
+  The paper fixes neither the split nor the scale granularity; the reading
+  taken here is 656 bytes per token:
+      bytes [0, 512)    E4M3 codes of the 512 latent columns
+      bytes [512, 528)  four little-endian IEEE binary32 scales, scale t
+                        covering latent columns [128 t, 128 t + 128)
+      bytes [528, 656)  the 64 RoPE columns as little-endian bf16
+  decoded as K[d] = e4m3(code[d]) * scale[d // 128] for d < 512 and
+  K[512 + r] = bf16(rope[r]).  (Scales are powers of two in the workloads;
+  the decoder does not depend on it.)
+
+All decoders are exact in float64.
 """
 import numpy as np
 
@@ -37,3 +51,16 @@ def e4m3_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     mag = np.where(exp == 0, subnormal, normal)
     mag = np.where((exp == 0xF) & (man == 7), np.nan, mag)
     return sign * mag
+
+
+DS_ROW_BYTES = 656
+
+
+def ds_rows_to_f64(rows: np.ndarray) -> np.ndarray:
+    """Latent-format rows (uint8 [n, 656]) -> float64 [n, 576]."""
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.uint8).reshape(-1, DS_ROW_BYTES))
+    codes = e4m3_bits_to_f64(r[:, :512])
+    scales = r[:, 512:528].copy().view('<f4').astype(np.float64)          # [n, 4]
+    rope_bits = r[:, 528:656].copy().view('<u2')                          # [n, 64]
+    latent = codes * np.repeat(scales, 128, axis=1)
+    return np.concatenate([latent, bf16_bits_to_f64(rope_bits)], axis=1)

@@ -11,7 +11,9 @@ and output row n = b*q + i:
   visible keys    j = 0 .. p                      (complete causal prefix)
   physical row    phys(b, j) = block_table[b, j // 64] * 64 + j % 64
   key row         K_j = decode(pool row phys(b, j))            (576 wide)
-                  (fp8 cache: K_j = e4m3(code) * scale[phys(b, j)])
+                  (fp8 cache: K_j = e4m3(code) * scale[phys(b, j)];
+                  latent-row cache: each 128-column latent tile has its
+                  own scale and the RoPE part is bf16, see formats)
   value row       V_j = K_j[0:512]                  (the latent; d_z = d_c)
   logit           z_j = sigma * <Q[n, h, :], K_j>   (sigma: the fp32 scale)
   log-sum-exp     lse = M + ln sum_j exp(z_j - M),  M = max_j z_j
@@ -23,7 +25,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .formats import bf16_bits_to_f64, e4m3_bits_to_f64
+from .formats import bf16_bits_to_f64, ds_rows_to_f64, e4m3_bits_to_f64
 
 PAGE = 64
 DIM_V = 512
@@ -42,6 +44,8 @@ def gather_history(kv, kv_scales, block_table, b, n_keys, kv_dtype):
     rows = flat[phys]
     if kv_dtype == 0:
         return bf16_bits_to_f64(rows)
+    if kv_dtype == 2:
+        return ds_rows_to_f64(rows)
     vals = e4m3_bits_to_f64(rows)
     scales = kv_scales.reshape(-1).astype(np.float64)[phys]
     return vals * scales[:, None]
@@ -85,7 +89,8 @@ def mla_attention(q, kv, block_table, seq_lens, q_chunk, softmax_scale,
     """Reference result for a whole batch (or a subset of requests / heads).
 
     q: uint16 bf16 bits [B*q_chunk, H, 576]; kv: uint16 [num_pages, 64, 576]
-    (bf16) or uint8 (e4m3) with kv_scales float32 [num_pages, 64].
+    (bf16) or uint8 (e4m3) with kv_scales float32 [num_pages, 64], or
+    (kv_dtype 2) uint8 latent-format rows [num_pages, 64, 656].
     ``key_ranges``: optional int array [B, 2]; restricts request b to keys
     [lo, hi) intersected with each row's causal prefix (a partial result over
     a slice of the history, as one split or one position shard computes).
@@ -156,6 +161,8 @@ def gather_positions(kv, kv_scales, block_table, b, positions, kv_dtype):
     rows = kv.reshape(-1, kv.shape[-1])[phys]
     if kv_dtype == 0:
         return bf16_bits_to_f64(rows)
+    if kv_dtype == 2:
+        return ds_rows_to_f64(rows)
     return e4m3_bits_to_f64(rows) * kv_scales.reshape(-1).astype(np.float64)[phys][:, None]
 
 

@@ -8,7 +8,7 @@ import numpy as np
 import torch
 
 from . import binding as B
-from .workloads import Batch, KV_FP8_E4M3
+from .workloads import Batch, KV_FP8_E4M3, KV_FP8_LATENT
 
 
 @dataclasses.dataclass
@@ -56,6 +56,9 @@ def to_device(batch: Batch, device: str = "cuda") -> DeviceBatch:
     if batch.kv_dtype == KV_FP8_E4M3:
         kv = torch.from_numpy(batch.kv).to(device)
         scales = torch.from_numpy(batch.kv_scales).to(device)
+    elif batch.kv_dtype == KV_FP8_LATENT:
+        kv = torch.from_numpy(batch.kv).to(device)
+        scales = None
     else:
         kv = torch.from_numpy(batch.kv.view(np.int16)).to(device).view(torch.bfloat16)
         scales = None

@@ -20,10 +20,17 @@ Recipe, one PCG64 stream per configuration, drawn in this order:
      ``num_pages = sum(ceil(s_b / 64))`` with no slack;
   3. the queries, ``standard_normal((B*q, H, 576), float32)``;
   4. ``perm = permutation(num_pages)``; request ``b``'s k-th page is
-     physical page ``perm[offset_b + k]``.
+     physical page ``perm[offset_b + k]``;
+  5. fp8 latent-row cache only: ``integers(-3, 3, (num_pages, 64, 4))``
+     (both ends included), an exponent per 128-column latent tile of each
+     row; the tile is multiplied by 2 to that power before encoding.
 Values are rounded to bf16 (round to nearest even) or, for the fp8 cache,
 encoded per token as OCP E4M3 ("fn": bias 7, max 448, no infinities) with one
-fp32 scale per token, ``scale = max|row| / 448``.
+fp32 scale per token, ``scale = max|row| / 448``, or, for the fp8 latent-row
+cache, packed into 656-byte rows: each 128-column tile of the latent encoded
+as E4M3 with its own scale, the smallest power of two not below
+``max|tile| / 448`` (so that no code saturates), and the RoPE part rounded
+to bf16.
 """
 from __future__ import annotations
 
@@ -39,6 +46,8 @@ SOFTMAX_SCALE = np.float32(1.0 / np.sqrt(192.0))   # 1/sqrt(d_n + d_r), d_n=128,
 
 KV_BF16 = 0
 KV_FP8_E4M3 = 1
+KV_FP8_LATENT = 2     # 656-byte rows: E4M3 latent, 4 fp32 tile scales, bf16 RoPE
+LATENT_ROW_BYTES = 656
 
 INT32_MAX = np.iinfo(np.int32).max
 
@@ -73,7 +82,7 @@ CONFIGS = {
 class Batch:
     """Host arrays of one batch; bit patterns, not values, for 16/8-bit data."""
     q: np.ndarray             # uint16 [B*q_chunk, H, 576]  (bf16 bits)
-    kv: np.ndarray            # uint16 [num_pages, 64, 576] (bf16) or uint8 (e4m3)
+    kv: np.ndarray            # uint16 [num_pages, 64, 576] (bf16), uint8 (e4m3) or uint8 [num_pages, 64, 656] (latent rows)
     kv_scales: Optional[np.ndarray]   # float32 [num_pages, 64] for e4m3, else None
     block_table: np.ndarray   # int32 [B, max_pages]
     seq_lens: np.ndarray      # int32 [B]
@@ -141,6 +150,25 @@ def encode_e4m3_per_token(rows: np.ndarray):
     return codes, scale
 
 
+def encode_fp8_latent_rows(rows: np.ndarray) -> np.ndarray:
+    """Pack ``[..., 576]`` float32 rows into 656-byte latent rows (uint8):
+    bytes [0, 512) E4M3 codes of the latent, [512, 528) four little-endian
+    fp32 tile scales (tile t = latent columns [128t, 128t + 128)), [528, 656)
+    the 64 RoPE values as little-endian bf16."""
+    lead = rows.shape[:-1]
+    tiles = rows[..., :DIM_V].reshape(*lead, 4, 128)
+    amax = np.max(np.abs(tiles), axis=-1).astype(np.float64)
+    expo = np.ceil(np.log2(np.where(amax > 0, amax / 448.0, 1.0)))
+    scale = np.ldexp(1.0, expo.astype(np.int32)).astype(np.float32)       # [..., 4], powers of two
+    codes = f32_to_e4m3_bits(tiles / scale[..., None]).reshape(*lead, DIM_V)
+    out = np.empty((*lead, LATENT_ROW_BYTES), dtype=np.uint8)
+    out[..., :512] = codes
+    out[..., 512:528] = np.ascontiguousarray(scale.astype('<f4')).view(np.uint8).reshape(*lead, 16)
+    rope = f32_to_bf16_bits(rows[..., DIM_V:]).astype('<u2')
+    out[..., 528:] = np.ascontiguousarray(rope).view(np.uint8).reshape(*lead, 128)
+    return out
+
+
 def draw_lengths(rng: np.random.Generator, spec: ConfigSpec) -> np.ndarray:
     kind = spec.lengths[0]
     if kind == "uniform":
@@ -180,6 +208,15 @@ def build_batch(rng: np.random.Generator, seq_lens, H: int, q_chunk: int,
         scales = None
     elif kv_dtype == KV_FP8_E4M3:
         kv, scales = encode_e4m3_per_token(pool)
+    elif kv_dtype == KV_FP8_LATENT:
+        # 5. (this format only) every 128-column latent tile of every row is
+        # multiplied by 2^u, u uniform in [-3, 3], so that tile scales differ
+        # within a row and across rows
+        u = rng.integers(-3, 3, size=(num_pages, PAGE, 4), endpoint=True)
+        pool[..., :DIM_V] *= np.repeat(np.ldexp(np.float32(1.0), u).astype(np.float32), 128, axis=-1)
+        kv = np.concatenate([encode_fp8_latent_rows(pool[i:i + 256]) for i in range(0, num_pages, 256)]) \
+            if num_pages else np.zeros((0, PAGE, LATENT_ROW_BYTES), np.uint8)
+        scales = None
     else:
         raise ValueError(kv_dtype)
     del pool
@@ -212,7 +249,8 @@ def make_custom(seq_lens, H: int, q_chunk: int = 1, kv_dtype: int = KV_BF16,
 
 def poison_unused_rows(batch: Batch) -> Batch:
     """Fill every pool row that no history reaches with NaN (bf16 0x7FC0 /
-    e4m3 0x7F, scale NaN).  Results must not change."""
+    e4m3 0x7F, scale NaN; latent rows: NaN codes, scales and RoPE).  Results
+    must not change."""
     kv = batch.kv.copy()
     scales = None if batch.kv_scales is None else batch.kv_scales.copy()
     used = np.zeros((batch.num_pages, PAGE), dtype=bool)
@@ -220,8 +258,13 @@ def poison_unused_rows(batch: Batch) -> Batch:
         s = int(batch.seq_lens[b])
         j = np.arange(s)
         used[batch.block_table[b, j // PAGE], j % PAGE] = True
-    nan_code = np.uint16(0x7FC0) if batch.kv_dtype == KV_BF16 else np.uint8(0x7F)
-    kv[~used] = nan_code
+    if batch.kv_dtype == KV_FP8_LATENT:
+        nan_row = np.full(LATENT_ROW_BYTES, 0x7F, dtype=np.uint8)              # E4M3 NaN codes
+        nan_row[512:528] = np.full(4, np.nan, dtype='<f4').view(np.uint8)      # NaN scales
+        nan_row[528:] = np.full(64, 0x7FC0, dtype='<u2').view(np.uint8)        # bf16 NaN
+        kv[~used] = nan_row
+    else:
+        kv[~used] = np.uint16(0x7FC0) if batch.kv_dtype == KV_BF16 else np.uint8(0x7F)
     if scales is not None:
         scales[~used] = np.float32(np.nan)
     return dataclasses.replace(batch, kv=kv, kv_scales=scales)
@@ -234,7 +277,7 @@ def workload_bytes_flops(batch: Batch):
     visible (query row, key)."""
     s = batch.seq_lens.astype(np.int64)
     q = batch.q_chunk
-    row_bytes = DIM_QK * 2 if batch.kv_dtype == KV_BF16 else DIM_QK + 4
+    row_bytes = {KV_BF16: DIM_QK * 2, KV_FP8_E4M3: DIM_QK + 4, KV_FP8_LATENT: LATENT_ROW_BYTES}[batch.kv_dtype]
     N = batch.B * q
     kv_bytes = int(s.sum()) * row_bytes
     other = (N * batch.H * DIM_QK * 2 + N * batch.H * DIM_V * 2 + N * batch.H * 4

@@ -288,6 +288,60 @@ def pin_fp8_dequant(seed=8):
     return worst
 
 
+def pin_latent_rows(seed=13):
+    """fp8 latent-row cache: attention equals torch's float64 SDPA over rows
+    decoded with torch's own dtypes (float8_e4m3fn codes times the tile's
+    float32 scale, bfloat16 RoPE), none of the oracle's decoders involved."""
+    batch = W.make_custom([70, 130], H=2, q_chunk=2, kv_dtype=W.KV_FP8_LATENT, seed=seed)
+    out, lse = oracle.mla_attention(batch.q, batch.kv, batch.block_table, batch.seq_lens, 2,
+                                    batch.softmax_scale, kv_dtype=2)
+    raw = torch.from_numpy(batch.kv.reshape(-1, 656).copy())
+    codes = raw[:, :512].contiguous().view(torch.float8_e4m3fn).to(torch.float64)
+    scales = raw[:, 512:528].contiguous().view(torch.float32).to(torch.float64)       # [rows, 4]
+    rope = raw[:, 528:].contiguous().view(torch.bfloat16).to(torch.float64)           # [rows, 64]
+    tbl = torch.cat([codes * scales.repeat_interleave(128, dim=1), rope], dim=1)
+    worst = 0.0
+    for b in range(batch.B):
+        s = int(batch.seq_lens[b])
+        rows = [int(batch.block_table[b, j // 64]) * 64 + j % 64 for j in range(s)]
+        k = tbl[rows]
+        qb = batch.q[b * 2:(b + 1) * 2]
+        qt = torch.from_numpy((qb.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+        qt = qt.permute(1, 0, 2).unsqueeze(0)
+        kt = k.unsqueeze(0).unsqueeze(0).expand(1, 2, s, 576)
+        vt = k[:, :512].unsqueeze(0).unsqueeze(0).expand(1, 2, s, 512)
+        mask = torch.arange(s).unsqueeze(0) <= (s - 2 + torch.arange(2).unsqueeze(1))
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            qt, kt, vt, attn_mask=mask, scale=float(batch.softmax_scale))[0].permute(1, 0, 2).numpy()
+        worst = max(worst, np.abs(out[b * 2:(b + 1) * 2] - ref).max())
+    return worst
+
+
+def latent_worked_row():
+    """One 656-byte latent row built by hand and its decoded values worked out
+    by hand: latent tile t has scale 2, 1/4, 8, 1/64; RoPE is bf16.
+    E4M3 codes used: 0x38 = +1.0 (exponent 7 = bias, mantissa 0), 0xB8 = -1.0,
+    0x3C = 1.5 (mantissa 4/8), 0x01 = 2^-9 (subnormal 1/8 * 2^-6), 0x7E = 448
+    (1.75 * 2^8), 0x00 = 0.  bf16 0x3F80 = 1.0, 0xC040 = -3.0."""
+    row = np.zeros(656, dtype=np.uint8)
+    row[0], row[1], row[130], row[300], row[511] = 0x38, 0xB8, 0x3C, 0x01, 0x7E
+    row[512:528] = np.array([2.0, 0.25, 8.0, 1.0 / 64.0], dtype='<f4').view(np.uint8)
+    row[528:530] = [0x80, 0x3F]        # rope[0] = 0x3F80, little-endian
+    row[654:656] = [0x40, 0xC0]        # rope[63] = 0xC040
+    expect = np.zeros(576)
+    expect[0], expect[1] = 2.0, -2.0          # tile 0, scale 2
+    expect[130] = 1.5 * 0.25                  # tile 1
+    expect[300] = 2.0 ** -9 * 8.0             # tile 2
+    expect[511] = 448.0 / 64.0                # tile 3
+    expect[512], expect[575] = 1.0, -3.0
+    return row, expect
+
+
+def pin_latent_worked_row():
+    row, expect = latent_worked_row()
+    return float(np.abs(oracle.ds_rows_to_f64(row[None, :])[0] - expect).max())
+
+
 def topk_lists(lens, q_chunk, rng, frac=0.4):
     """Distinct visible positions for every row (a random subset, shuffled),
     padded with -1 to a common length; returns idx [N, k] and count [N]."""

@@ -17,6 +17,7 @@ import torch
 import oracle
 import oracle.formats
 import oracle.mla
+from paper_2609_37626_amd import workloads as W
 from tests import oracle_pins as pins
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -73,6 +74,27 @@ def test_matches_torch_sdpa_float64_with_causal_chunk_mask():
 
 def test_fp8_cache_matches_sdpa_on_dequantised_rows():
     assert pins.pin_fp8_dequant() <= 1e-12
+
+
+def test_latent_row_cache_matches_sdpa_on_torch_decoded_rows():
+    assert pins.pin_latent_rows() <= 1e-12
+
+
+def test_latent_row_hand_decoded():
+    assert pins.pin_latent_worked_row() == 0.0
+
+
+def test_latent_rows_of_power_of_two_scales_are_bf16_exact():
+    # with power-of-two tile scales every decoded value is a bf16 value: the
+    # latent-row cache then equals a bf16 cache holding the same numbers
+    batch = W.make_custom([70, 130], H=2, q_chunk=2, kv_dtype=W.KV_FP8_LATENT, seed=14)
+    K = oracle.ds_rows_to_f64(batch.kv.reshape(-1, 656))
+    bits = (K.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal(oracle.bf16_bits_to_f64(bits), K)
+    a = oracle.mla_attention(batch.q, batch.kv, batch.block_table, batch.seq_lens, 2, batch.softmax_scale, kv_dtype=2)
+    b = oracle.mla_attention(batch.q, bits.reshape(-1, 64, 576), batch.block_table, batch.seq_lens, 2,
+                             batch.softmax_scale, kv_dtype=0)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
 
 
 def test_single_key_returns_its_latent():
@@ -207,6 +229,28 @@ def _merge_flipped(parts_out, parts_lse):
     return out, -L
 
 
+def _latent_tile_of_64(rows):
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.uint8).reshape(-1, 656))
+    codes = oracle.formats.e4m3_bits_to_f64(r[:, :512])
+    scales = r[:, 512:528].copy().view('<f4').astype(np.float64)
+    latent = codes * np.tile(np.repeat(scales, 64, axis=1), 2)       # tiles of 64 columns
+    return np.concatenate([latent, oracle.formats.bf16_bits_to_f64(r[:, 528:].copy().view('<u2'))], axis=1)
+
+
+def _latent_rope_big_endian(rows):
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.uint8).reshape(-1, 656))
+    codes = oracle.formats.e4m3_bits_to_f64(r[:, :512])
+    scales = r[:, 512:528].copy().view('<f4').astype(np.float64)
+    latent = codes * np.repeat(scales, 128, axis=1)
+    return np.concatenate([latent, oracle.formats.bf16_bits_to_f64(r[:, 528:].copy().view('>u2'))], axis=1)
+
+
+def _latent_scales_ignored(rows):
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.uint8).reshape(-1, 656))
+    latent = oracle.formats.e4m3_bits_to_f64(r[:, :512])
+    return np.concatenate([latent, oracle.formats.bf16_bits_to_f64(r[:, 528:].copy().view('<u2'))], axis=1)
+
+
 MUTANTS = {
     "causal limit one too far": ("attention_rows", _rows_mask_plus_one),
     "causal limit one short": ("attention_rows", _rows_mask_minus_one),
@@ -219,6 +263,9 @@ MUTANTS = {
     "bf16 exponent bias off by one": ("bf16", _bf16_bias_off),
     "e4m3 read as fnuz (bias 8)": ("e4m3", _e4m3_fnuz_bias),
     "merge weights of wrong sign": ("merge_partials", _merge_flipped),
+    "latent tile scale per 64 columns": ("ds_rows", _latent_tile_of_64),
+    "latent-row RoPE read big-endian": ("ds_rows", _latent_rope_big_endian),
+    "latent tile scales ignored": ("ds_rows", _latent_scales_ignored),
 }
 
 
@@ -230,6 +277,7 @@ def _planted(kind, fn):
         "bf16": [(oracle.mla, "bf16_bits_to_f64"), (oracle, "bf16_bits_to_f64")],
         "e4m3": [(oracle.mla, "e4m3_bits_to_f64"), (oracle, "e4m3_bits_to_f64")],
         "merge_partials": [(oracle.mla, "merge_partials"), (oracle, "merge_partials")],
+        "ds_rows": [(oracle.mla, "ds_rows_to_f64"), (oracle, "ds_rows_to_f64")],
     }[kind]
     saved = [(mod, name, getattr(mod, name)) for mod, name in targets]
     try:
@@ -246,6 +294,8 @@ def _pins_all_pass():
         (pins.pin_brute_force, TOL),
         (pins.pin_sdpa, 1e-12),
         (pins.pin_fp8_dequant, 1e-12),
+        (pins.pin_latent_rows, 1e-12),
+        (pins.pin_latent_worked_row, 0.0),
         (pins.pin_single_key, 0.0),
         (pins.pin_zero_query, TOL),
         (pins.pin_one_hot, TOL),
