@@ -64,6 +64,17 @@ extern "C" {
 /* ---- cache formats --------------------------------------------------------- */
 #define SPLASH_KV_BF16      0  /* pool: [num_pages, 64, 576] bf16 */
 #define SPLASH_KV_FP8_E4M3  1  /* pool: [num_pages, 64, 576] OCP E4M3 ("fn") bytes + kv_scales [num_pages, 64] fp32 */
+/* Latent-row cache (App. B, theoretical scenarios for DCU and H200,
+ * residency assumptions: FP8 latent with its scales and BF16 RoPE; the
+ * paper fixes neither the split nor the scale granularity).  Pool:
+ * [num_pages, 64, 656] bytes; a row is 512 OCP E4M3 latent codes, four
+ * little-endian fp32 scales (scale t covers latent columns [128t, 128t+128))
+ * and the 64 RoPE values as bf16: K[d] = e4m3(code[d]) * scale[d / 128] for
+ * d < 512, K[512 + r] = rope[r].  Scales must be powers of two (finite,
+ * nonzero; NaN rows only where no history reaches); kv_scales is ignored.
+ * splash_mla_attend, splash_mla_attend_shard and the gather take it; the
+ * top-k variant returns SPLASH_ERR_UNSUPPORTED. */
+#define SPLASH_KV_FP8_LATENT 2
 
 /* ---- flags ------------------------------------------------------------------ */
 #define SPLASH_FLAG_DEBUG_CHECK  1u  /* validate seq_lens / block table on the device first; synchronises `stream` */
@@ -84,7 +95,7 @@ typedef struct splash_mla_desc {
     int32_t max_pages_per_seq;  /* row stride of block_table (>= ceil(max s_b / 64)) */
     int32_t num_pages;          /* pages in the pool */
     int32_t kv_dtype;           /* SPLASH_KV_* */
-    const float* kv_scales;     /* device [num_pages, 64] fp32 per-token scales; FP8 only, else ignored */
+    const float* kv_scales;     /* device [num_pages, 64] fp32 per-token scales; SPLASH_KV_FP8_E4M3 only, else ignored */
     float softmax_scale;        /* multiplies <q, k>; finite and > 0 (1/sqrt(192) for DeepSeek-V3 dims) */
     uint32_t flags;             /* SPLASH_FLAG_* */
     int32_t split_pages;        /* with SPLASH_FLAG_FORCE_SPLIT: pages per work unit, >= 1 */
@@ -283,7 +294,7 @@ int splash_mla_combine(const float* partials, const float* partial_lse,
  * splash_mla_debug_gather (tests): copy every history, token by token, into
  * a dense buffer through the same page-address code the attention kernel
  * uses.  dense_out holds sum_b seq_lens[b] rows of the pool's row bytes
- * (1152 for bf16, 576 for fp8), request after request.
+ * (1152 for bf16, 576 for fp8, 656 for latent rows), request after request.
  */
 int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table,
                             const int32_t* seq_lens, const splash_mla_desc* desc,

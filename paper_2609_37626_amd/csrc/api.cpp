@@ -104,7 +104,7 @@ int validate_desc(const splash_mla_desc* d, int32_t q_chunk) {
   if (d->page_size != kPage) return fail(SPLASH_ERR_UNSUPPORTED, "page_size must be 64 (got %d)", d->page_size);
   if (d->num_heads < 16 || d->num_heads > kMaxHeads || d->num_heads % 16)
     return fail(SPLASH_ERR_UNSUPPORTED, "num_heads must be a multiple of 16 in [16,128] (got %d)", d->num_heads);
-  if (d->kv_dtype != SPLASH_KV_BF16 && d->kv_dtype != SPLASH_KV_FP8_E4M3)
+  if (d->kv_dtype != SPLASH_KV_BF16 && d->kv_dtype != SPLASH_KV_FP8_E4M3 && d->kv_dtype != SPLASH_KV_FP8_LATENT)
     return fail(SPLASH_ERR_UNSUPPORTED, "unknown kv_dtype %d", d->kv_dtype);
   if (d->kv_dtype == SPLASH_KV_FP8_E4M3 && !d->kv_scales)
     return fail(SPLASH_ERR_INVALID_ARGUMENT, "fp8 cache needs kv_scales");
@@ -397,6 +397,8 @@ int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* b
                            const splash_mla_desc* desc, void* workspace, size_t ws_bytes, void* stream) {
   int st = validate_desc(desc, q_chunk);
   if (st != SPLASH_OK) return st;
+  if (desc->kv_dtype == SPLASH_KV_FP8_LATENT)
+    return fail(SPLASH_ERR_UNSUPPORTED, "the top-k variant reads bf16 or per-token fp8 caches");
   if (desc->batch == 0) return SPLASH_OK;
   if (!topk_idx || !topk_count) return fail(SPLASH_ERR_INVALID_ARGUMENT, "topk_idx and topk_count must be non-NULL");
   if (topk < 1 || topk > (1 << 24)) return fail(SPLASH_ERR_INVALID_ARGUMENT, "topk must be in [1, 2^24] (got %d)", topk);
@@ -513,7 +515,8 @@ int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table, co
     return fail(SPLASH_ERR_INVALID_ARGUMENT, "kv_pages, block_table, seq_lens and dense_out must be non-NULL");
   if (!aligned16(kv_pages) || !aligned16(dense_out))
     return fail(SPLASH_ERR_MISALIGNED, "kv_pages and dense_out must be 16-byte aligned");
-  const int32_t row_bytes = desc->kv_dtype == SPLASH_KV_FP8_E4M3 ? kDimQK : 2 * kDimQK;
+  const int32_t row_bytes = desc->kv_dtype == SPLASH_KV_FP8_LATENT ? kLatentRowBytes
+                            : desc->kv_dtype == SPLASH_KV_FP8_E4M3 ? kDimQK : 2 * kDimQK;
   hipError_t e = launch_gather(kv_pages, block_table, seq_lens, desc->batch, desc->max_pages_per_seq, row_bytes,
                                dense_out, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SPLASH_OK : hip_fail(e, "gather launch");

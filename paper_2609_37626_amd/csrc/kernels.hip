@@ -555,18 +555,23 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
 // so every 1 KB direct-to-LDS instruction reads whole memory lines of 8 (16)
 // rows, and the XOR spreads the operand reads over the LDS banks.
 
-template <bool FP8>
+//
+// Latent rows (LAT: 656 B = 512 E4M3 codes at 0 | 4 fp32 tile scales at 512
+// | 64 bf16 RoPE at 528): in LDS the latent's 8 line groups as fp8, then the
+// RoPE as one bf16 line group at kRopeOff, then the rows' tile scales (16 B
+// per row) at kData.
+template <bool FP8, bool LAT = false>
 struct StepLayout {
-  static constexpr int kRowBytes = FP8 ? kDimQK : 2 * kDimQK;       // 576 / 1152
-  static constexpr int kGroupBytes = FP8 ? 64 : 128;                 // memory line group
-  static constexpr int kGroupStride = kStepKeys * kGroupBytes;       // 2048 / 4096
-  static constexpr int kData = kStepKeys * kRowBytes;                // 18432 / 36864
-  static constexpr int kBuf = FP8 ? kData + 256 : kData;             // + fp32 scales
+  static constexpr int kRowBytes = LAT ? 656 : FP8 ? kDimQK : 2 * kDimQK;   // 656 / 576 / 1152
+  static constexpr int kRopeOff = 8 * kStepKeys * 64;                      // LAT: 16384
+  static constexpr int kData = LAT ? kRopeOff + kStepKeys * 128 : kStepKeys * kRowBytes;  // 20480 / 18432 / 36864
+  static constexpr int kBuf = LAT ? kData + 1024 : FP8 ? kData + 256 : kData;             // + fp32 scales
   // Ring slots: the step being multiplied (QK), the previous one (PV), and
   // kDist steps in flight.
   static constexpr int kSlots = FP8 ? 4 : 3;
   static constexpr int kDist = kSlots - 2;
-  static constexpr int kLoadsPerStep = FP8 ? 5 : 9;                  // per wave
+  // per wave and step (LAT: wave 0; waves 1-3 issue one fewer)
+  static constexpr int kLoadsPerStep = LAT ? 6 : FP8 ? 5 : 9;
   static constexpr int kRing = kSlots * kBuf;
 };
 
@@ -623,12 +628,31 @@ __device__ __forceinline__ void dma_b32(const void* sbase, uint32_t voff, const 
 //  bf16: wave w loads rows [8w, 8w+8) of every line group g (t = g);
 //  fp8:  instruction i = w + 4t (< 18) loads line group i >> 1, rows
 //        [16 (i & 1), +16); waves 2 and 3 also load the 32 token scales.
+//  LAT:  t < 4 as fp8 (the latent's 8 line groups); t = 4: wave w loads the
+//        RoPE of rows [8w, 8w+8) into the bf16 layout; t = 5: wave 0 loads
+//        the 32 rows' tile scales.
 // step_src / step_scales are uniform; src_lane is the lane's byte offset
 // inside the step for t = 0.
-template <bool FP8, int t>
+template <bool FP8, int t, bool LAT = false>
 __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                           uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
-  if constexpr (!FP8) {
+  if constexpr (LAT) {
+    using L = StepLayout<true, true>;
+    if constexpr (t < 4) {
+      dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+    } else {
+      // lane id from an asm (volatile: recomputed here, not held in a
+      // register across the loop), then the lane's source offset
+      uint32_t ln;
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+      if constexpr (t == 4) {
+        const uint32_t r = 8 * wave + (ln >> 3);
+        dma_b128(step_src, r * L::kRowBytes + 528 + (((ln & 7) ^ ((r >> 1) & 7)) * 16), buf + L::kRopeOff + 1024 * wave);
+      } else if (wave == 0) {
+        dma_b128(step_src, (ln & 31) * L::kRowBytes + 512, buf + L::kData);  // lanes 32-63 repeat 0-31
+      }
+    }
+  } else if constexpr (!FP8) {
     dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 1024 * wave);
   } else {
     if (t < 4 || wave + 4 * t < 18) {
@@ -665,19 +689,19 @@ __device__ __forceinline__ void issue_from_v(uint64_t row_addr, uint64_t scale_a
   }
 }
 
-template <bool FP8, int t = 0>
+template <bool FP8, bool LAT, int t = 0>
 __device__ __forceinline__ void issue_from(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                            uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
-  if constexpr (t < StepLayout<FP8>::kLoadsPerStep) {
-    issue_one<FP8, t>(step_src, step_scales, src_lane, buf, wave);
-    issue_from<FP8, t + 1>(step_src, step_scales, src_lane, buf, wave);
+  if constexpr (t < StepLayout<FP8, LAT>::kLoadsPerStep) {
+    issue_one<FP8, t, LAT>(step_src, step_scales, src_lane, buf, wave);
+    issue_from<FP8, LAT, t + 1>(step_src, step_scales, src_lane, buf, wave);
   }
 }
 
-template <bool FP8>
+template <bool FP8, bool LAT>
 __device__ __forceinline__ void issue_step(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                            uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
-  issue_from<FP8>(step_src, step_scales, src_lane, buf, wave);
+  issue_from<FP8, LAT>(step_src, step_scales, src_lane, buf, wave);
 }
 
 // QK^T MFMAs are issued through inline asm with a VGPR accumulator: the
@@ -760,6 +784,41 @@ __device__ __forceinline__ bf16x8 frag_bf16(const FragRaw<FP8>& r) {
   else return r;
 }
 
+// Latent rows: 8 E4M3 codes of one latent tile times the tile's scale.  The
+// conversion applies only the scale operand's exponent (2^floor(log2 s)),
+// which is why the format requires power-of-two scales; the products are
+// then exact in bf16.
+__device__ __forceinline__ bf16x8 fp8x8_scaled_to_bf16(u32x2 raw, float scale) {
+  u32x4 r;
+  r[0] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[0], scale, false));
+  r[1] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[0], scale, true));
+  r[2] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[1], scale, false));
+  r[3] = __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)raw[1], scale, true));
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+// Latent rows: a wave's PV covers output columns [128 wave, +128), one
+// latent tile, so the tile scale of each key multiplies that key's P weight
+// instead of V.  s[e] is the scale of the key of fragment element e.
+__device__ __forceinline__ bf16x8 scale_p(bf16x8 p, const float (&s)[8]) {
+  const u32x4 w = __builtin_bit_cast(u32x4, p);
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    r[i] = pack_bf16x2(__builtin_bit_cast(float, w[i] << 16) * s[2 * i],
+                       __builtin_bit_cast(float, w[i] & 0xffff0000u) * s[2 * i + 1]);
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+// Latent rows: the tile-`wave` scales of the 8 keys of the P^T fragment
+// (key half kh) a lane reads; element e is key 16kh + 8(e >> 2) + 4h + (e & 3)
+// (the slot order of the P exchange).
+__device__ __forceinline__ void load_p_scales(const uint8_t LDS_AS* scales, int kh, int h, int wave, float (&s)[8]) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    s[e] = *(const float LDS_AS*)(scales + 16 * (16 * kh + 8 * (e >> 2) + 4 * h + (e & 3)) + 4 * wave);
+}
+
 // P^T operand fragment (head block hb, key half kh) from the P exchange area:
 // head hh's 32 weights are 64 B, slot (kh, half) at ((2kh + half) ^ (hh>>2 & 3)) * 16.
 __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t half) {
@@ -769,15 +828,22 @@ __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t ha
 // PV of one 32-key step as a standalone MFMA stream (the unit's last step,
 // which has no QK to interleave with): 32 MFMAs,
 // o[cbl][hb] += V^T(cb = 4*wave + cbl, kh) P^T(hb, kh) with V from `vbuf` and
-// P from the P exchange area.
-template <bool FP8>
+// P from the P exchange area (LAT: P scaled by the keys' tile scales, which
+// sit at vbuf + lat_scales).
+template <bool FP8, bool LAT = false>
 __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint32_t (*vbase)[2],
                                           const uint8_t LDS_AS* p_lds, int wave, int n32, int h,
-                                          f32x16 (&o)[4][4]) {
+                                          f32x16 (&o)[4][4], int lat_scales = 0) {
   // V fragments are double-buffered one column block ahead (c = 4kh + cbl).
   bf16x8 pf[4], vf[2];
+  float psc[8];
+  if constexpr (LAT) load_p_scales(vbuf + lat_scales, 0, h, wave, psc);
 #pragma unroll
-  for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 0, h));
+  for (int hb = 0; hb < 4; ++hb) {
+    pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 0, h));
+    if constexpr (LAT) pf[hb] = scale_p(pf[hb], psc);
+  }
+  if constexpr (LAT) load_p_scales(vbuf + lat_scales, 1, h, wave, psc);
   vf[0] = load_v_frag<FP8>(vbuf, vbase, 4 * wave, 0);
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
@@ -791,7 +857,10 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
     o[cbl][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c & 1], pf[hb], o[cbl][hb], 0, 0, 0);
     // P fragments of key half 1 replace those of half 0 once the last MFMA
     // of half 0 that reads them has been issued
-    if (kh == 0 && cbl == 3) pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 1, h));
+    if (kh == 0 && cbl == 3) {
+      pf[hb] = *(const bf16x8 LDS_AS*)(p_lds + p_slot(32 * hb + n32, 1, h));
+      if constexpr (LAT) pf[hb] = scale_p(pf[hb], psc);
+    }
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -801,10 +870,14 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
 // covers list entries [64 p0, 64 p1) instead of pages, and its prologue
 // resolves every entry to its pool row (into the LDS the block-table slice
 // uses otherwise), from which each lane loads its staged row.
-template <bool FP8, bool TOPK>
+// LAT: the fp8 latent-row cache (FP8 set too): latent tiles converted with
+// their tile scale for QK, the RoPE read as bf16, and for PV each wave's P
+// scaled by its tile's key scales.
+template <bool FP8, bool TOPK, bool LAT = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
-  using L = StepLayout<FP8>;
+  static_assert(!LAT || (FP8 && !TOPK), "latent rows: dense fp8 variant only");
+  using L = StepLayout<FP8, LAT>;
   constexpr int kPOff = L::kRing;                    // P exchange area, two steps
   constexpr int kLOff = kPOff + 2 * kPBytes;         // per-head normaliser, 128 floats
   constexpr int kBtOff = kLOff + kMaxHeads * 4;      // block-table slice (top-k: the unit's pool rows)
@@ -837,19 +910,22 @@ void attend_kernel(AttendLaunch a) {
     dma_slot = 1024 * wave + 16 * lane;              // + 4096 t
   } else {
     dma_row = 16 * (wave & 1) + (lane >> 2);
-    src_lane = dma_row * 576 + 64 * (wave >> 1) + (((lane & 3) ^ ((dma_row >> 1) & 3)) * 16);
+    src_lane = dma_row * L::kRowBytes + 64 * (wave >> 1) + (((lane & 3) ^ ((dma_row >> 1) & 3)) * 16);
     dma_slot = 2048 * (wave >> 1) + 1024 * (wave & 1) + 16 * lane;   // + 4096 t
   }
   // K operand of k-step ks (dims 16ks + 8h + [0, 8)): row n32, chunk
   // 2(ks & 3) + h of line group ks >> 2 (bf16), or 16-byte chunk ks & 3, half
   // h (fp8); kbase[ks & 3] + G * (ks >> 2) addresses it (G = group stride).
-  uint32_t kbase[4];
+  // LAT: the RoPE k-steps 32..35 read the bf16 line group at kRopeOff
+  // through kbase_r (the bf16 formula).
+  uint32_t kbase[4], kbase_r[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     if constexpr (!FP8)
       kbase[m] = n32 * 128 + (((2 * m + h) ^ ((n32 >> 1) & 7)) * 16);
     else
       kbase[m] = n32 * 64 + ((m ^ ((n32 >> 1) & 3)) * 16) + 8 * h;
+    kbase_r[m] = L::kRopeOff + n32 * 128 + (((2 * m + h) ^ ((n32 >> 1) & 7)) * 16);
   }
   // V operand (transposing reads), see load_v_frag
   const int i16 = lane & 15, g16 = lane >> 4;
@@ -943,10 +1019,10 @@ void attend_kernel(AttendLaunch a) {
 
     auto step_src = [&](int j, int phys) {
       const int key = key_begin + j * kStepKeys;
-      return kv + (size_t)phys * (kPage * L::kRowBytes) + (size_t)((key >> 5) & 1) * L::kData;
+      return kv + (size_t)phys * (kPage * L::kRowBytes) + (size_t)((key >> 5) & 1) * (kStepKeys * L::kRowBytes);
     };
     auto step_scales = [&](int j, int phys) -> const float* {
-      if constexpr (!FP8) return nullptr;
+      if constexpr (!FP8 || LAT) return nullptr;
       const int key = key_begin + j * kStepKeys;
       return a.kv_scales + (size_t)phys * kPage + ((key >> 5) & 1) * kStepKeys;
     };
@@ -987,7 +1063,7 @@ void attend_kernel(AttendLaunch a) {
             issue_from_v<FP8>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave);
           } else {
             const int ph = step_phys(j);
-            issue_step<FP8>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
+            issue_step<FP8, LAT>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
           }
         }
 
@@ -1029,19 +1105,31 @@ void attend_kernel(AttendLaunch a) {
           pf_srow = scale_addr(j == 0 ? next_srow : next_srow_v);
         }
         uint8_t LDS_AS* pf_buf = slot_buf(j + L::kDist);
-        if (L::kDist == 2 && j + 1 < nsteps) wait_vmcnt<L::kLoadsPerStep>();
-        else wait_vmcnt<0>();
+        if (L::kDist == 2 && j + 1 < nsteps) {
+          // (LAT: only wave 0 loads the tile scales)
+          if (LAT && wave != 0) wait_vmcnt<L::kLoadsPerStep - 1>();
+          else wait_vmcnt<L::kLoadsPerStep>();
+        } else {
+          wait_vmcnt<0>();
+        }
         if (valid < kStepKeys) {
           // rows past the history end: P is zero there, V must not be NaN
           const u32x4 z = {0, 0, 0, 0};
           if ((int)opaque(dma_row) >= valid) {
 #pragma unroll
             for (int t = 0; t < L::kLoadsPerStep; ++t)
-              if (!FP8 || t < 4 || wave + 4 * t < 18) *(u32x4 LDS_AS*)(buf + dma_slot + 4096 * t) = z;
+              if (!FP8 || t < 4 || (!LAT && wave + 4 * t < 18)) *(u32x4 LDS_AS*)(buf + dma_slot + 4096 * t) = z;
           }
-          // their token scales too (both waves that load the scales clear
-          // them after their own loads landed, so a zero is written last)
-          if constexpr (FP8) {
+          if constexpr (LAT) {
+            // their RoPE and tile scales (each cleared by the wave that
+            // loaded it, after its own loads landed): zero scales keep the
+            // scaled P and K finite
+            if ((int)opaque(8 * wave + (lane >> 3)) >= valid)
+              *(u32x4 LDS_AS*)(buf + L::kRopeOff + 1024 * wave + 16 * lane) = z;
+            if (wave == 0 && (int)(lane & 31) >= valid) *(u32x4 LDS_AS*)(buf + L::kData + 16 * lane) = z;
+          } else if constexpr (FP8) {
+            // their token scales too (both waves that load the scales clear
+            // them after their own loads landed, so a zero is written last)
             if (wave >= 2 && (int)(lane & 31) >= valid) *(float LDS_AS*)(buf + L::kData + 4 * lane) = 0.f;
           }
         }
@@ -1057,15 +1145,23 @@ void attend_kernel(AttendLaunch a) {
         constexpr int kPV1 = 8;
         f32x16 sacc;
         bf16x8 pf[4], pf1[4];
+        float psc[2][8];  // LAT: tile-`wave` scales of the keys of pf / pf1
         FragRaw<FP8> vf[3];  // V fragments of three column blocks, as read
         bf16x8 vcur;         // that of the current column block, converted
         {
           constexpr int kKPre = 4;  // K fragments in flight
           FragRaw<FP8> kf[kKPre];
           bf16x8 ka_prev;  // fp8: the converted fragment the previous QK MFMA was issued with
+          bf16x8 kr[4];    // LAT: the RoPE fragments, bf16 as staged
+          f32x4 tsc;       // LAT: tile scales of this lane's key row
+          if constexpr (LAT) tsc = *(const f32x4 LDS_AS*)(buf + L::kData + 16 * n32);
 #pragma unroll
           for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_raw<FP8>(buf, kbase, ks);
           if constexpr (kPV) {
+            if constexpr (LAT) {
+              load_p_scales(vbuf + L::kData, 0, h, wave, psc[0]);
+              load_p_scales(vbuf + L::kData, 1, h, wave, psc[1]);
+            }
 #pragma unroll
             for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 0, h));
             vf[0] = load_v_raw<FP8>(vbuf, vbase, 4 * wave, 0);
@@ -1083,7 +1179,9 @@ void attend_kernel(AttendLaunch a) {
               const int cn = (q >> 2) + 2;
               vf[cn % 3] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
-            const bf16x8 ka = frag_bf16<FP8>(kf[i % kKPre]);
+            bf16x8 ka;
+            if constexpr (LAT) ka = i < 32 ? fp8x8_scaled_to_bf16(kf[i % kKPre], tsc[i >> 3]) : kr[i & 3];
+            else ka = frag_bf16<FP8>(kf[i % kKPre]);
             if constexpr (FP8) {
               // the conversion must not reuse the registers of the MFMA just
               // issued (the asm hides that read from the compiler): keeping
@@ -1091,11 +1189,19 @@ void attend_kernel(AttendLaunch a) {
               if (i > 0) asm volatile("" ::"v"(ka), "v"(ka_prev));
               ka_prev = ka;
             }
-            if (i + kKPre < 36) kf[i % kKPre] = load_k_raw<FP8>(buf, kbase, i + kKPre);
+            if (i + kKPre < 36) {
+              if (LAT && i + kKPre >= 32) kr[(i + kKPre) & 3] = *(const bf16x8 LDS_AS*)(buf + kbase_r[(i + kKPre) & 3]);
+              else kf[i % kKPre] = load_k_raw<FP8>(buf, kbase, i + kKPre);
+            }
             if (i == 0) mfma_qk<true, FP8>(sacc, ka, qf[i]);
             else mfma_qk<false, FP8>(sacc, ka, qf[i]);
             if (q != kNone) {
               const int c = q >> 2, hb = q & 3;
+              if constexpr (LAT) {
+                // P scaled at its first use (its 4 column blocks share it)
+                if (c == 0) pf[hb] = scale_p(pf[hb], psc[0]);
+                if (c == 4) pf1[hb] = scale_p(pf1[hb], psc[1]);
+              }
               const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
               if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
               o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
@@ -1119,15 +1225,15 @@ void attend_kernel(AttendLaunch a) {
                 }
               } else {
                 switch (i >> 2) {
-                  case 0: issue_one<FP8, 0>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 1: issue_one<FP8, 1>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 2: issue_one<FP8, 2>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 3: issue_one<FP8, 3>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 4: issue_one<FP8, 4>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 5: issue_one<FP8, 5>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 6: issue_one<FP8, 6>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 7: issue_one<FP8, 7>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  default: issue_one<FP8, 8>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 0: issue_one<FP8, 0, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 1: issue_one<FP8, 1, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 2: issue_one<FP8, 2, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 3: issue_one<FP8, 3, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 4: issue_one<FP8, 4, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 5: issue_one<FP8, 5, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 6: issue_one<FP8, 6, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 7: issue_one<FP8, 7, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  default: issue_one<FP8, 8, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
                 }
               }
             }
@@ -1143,6 +1249,9 @@ void attend_kernel(AttendLaunch a) {
               const int cn = c + 2;
               vf[cn % 3] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
+            if constexpr (LAT) {
+              if (c == 4) pf1[hb] = scale_p(pf1[hb], psc[1]);
+            }
             const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
             if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
             o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
@@ -1157,7 +1266,7 @@ void attend_kernel(AttendLaunch a) {
         constexpr int kLead = kPV ? 2 : 0, kTail = kPV ? 2 : 0;
         constexpr int kN2 = kPV ? 32 - kPV1 - kTail : 0;  // PV slots of stream 2
         f32x2 sc[8];
-        if constexpr (FP8) {
+        if constexpr (FP8 && !LAT) {
 #pragma unroll
           for (int r = 0; r < 16; r += 2) {
             const int m = 8 * (r >> 2) + 4 * h + (r & 3);
@@ -1177,7 +1286,7 @@ void attend_kernel(AttendLaunch a) {
         // head, keys 8(r>>2)+4h+(r&3); t = z*log2(e) - m_ref.
         auto finish_scores = [&]() {
           wait_mfma_vgpr(sacc);
-          if constexpr (FP8) {
+          if constexpr (FP8 && !LAT) {
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
               sacc[r] *= sc[r >> 1][0];
@@ -1219,7 +1328,7 @@ void attend_kernel(AttendLaunch a) {
           if (r & 1) {
             // largest t of the pass, two per max3
             tmax = fmaxf(tmax, fmaxf(tlo, t));
-            if constexpr (FP8) {
+            if constexpr (FP8 && !LAT) {
               // the token scale multiplies V too: fold it into the weight
               pb[r >> 1] = pack_bf16x2(plo * sc[r >> 1][0], p * sc[r >> 1][1]);
             } else {
@@ -1233,7 +1342,7 @@ void attend_kernel(AttendLaunch a) {
           }
           // keep the element here, between the MFMAs of its slot, instead of
           // letting the compiler sink the whole softmax below the stream
-          if constexpr (FP8) asm volatile("" : "+v"(pexact));
+          if constexpr (FP8 && !LAT) asm volatile("" : "+v"(pexact));
           else asm volatile("" : "+v"(pexact), "+v"(psum));
         };
         if constexpr (kPV) {
@@ -1256,7 +1365,7 @@ void attend_kernel(AttendLaunch a) {
           for (int r = 0; r < 16; ++r) softmax_elem(r);
         }
         l_exact += pexact;
-        l_run += FP8 ? pexact : psum;
+        l_run += (FP8 && !LAT) ? pexact : psum;
         // publish this wave's P^T (keys in slot order) for every wave's PV
         uint8_t LDS_AS* p_cur = p_lds + kPBytes * (j & 1);
         *(u32x4 LDS_AS*)(p_cur + p_slot(head, 0, h)) = (u32x4){pb[0], pb[1], pb[2], pb[3]};
@@ -1273,7 +1382,7 @@ void attend_kernel(AttendLaunch a) {
       for (int j = 1; j < nsteps; ++j) qk_softmax(j, std::true_type{});
       // PV of the last step
       lds_barrier();
-      pv_stream<FP8>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o);
+      pv_stream<FP8, LAT>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o, L::kData);
       const float mt_max = fmaxf(tmax, wave_xor32(tmax));
       const float m_seen = m_ref + mt_max;
       const bool over = mt_max > 64.0f;
@@ -1663,7 +1772,9 @@ hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
 }
 
 hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) {
-  if (a.kv_dtype == 1) {
+  if (a.kv_dtype == 2) {
+    hipLaunchKernelGGL((attend_kernel<true, false, true>), dim3(workers), dim3(256), 0, s, a);
+  } else if (a.kv_dtype == 1) {
     if (a.topk_idx) {
       hipLaunchKernelGGL((attend_kernel<true, true>), dim3(workers), dim3(256), 0, s, a);
     } else {

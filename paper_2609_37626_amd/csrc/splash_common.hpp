@@ -17,6 +17,7 @@ namespace splash {
 constexpr int kPage = 64;          // tokens per page
 constexpr int kDimQK = 576;        // latent 512 + rope 64 (d_q = d_c + d_r)
 constexpr int kDimV = 512;         // d_z = d_c
+constexpr int kLatentRowBytes = 656;  // fp8 latent-row cache: 512 E4M3 + 4 fp32 tile scales + 64 bf16 RoPE
 constexpr int kMaxHeads = 128;
 constexpr int kStepKeys = 32;      // keys per pipeline step (half a page)
 constexpr int kMaxUnitPages = 1024;  // the block-table slice of one unit is staged in LDS

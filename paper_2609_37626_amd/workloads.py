@@ -21,7 +21,7 @@ Recipe, one PCG64 stream per configuration, drawn in this order:
   3. the queries, ``standard_normal((B*q, H, 576), float32)``;
   4. ``perm = permutation(num_pages)``; request ``b``'s k-th page is
      physical page ``perm[offset_b + k]``;
-  5. fp8 latent-row cache only: ``integers(-3, 3, (num_pages, 64, 4))``
+  5. fp8 latent-row cache only: ``integers(-3, 0, (num_pages, 64, 4))``
      (both ends included), an exponent per 128-column latent tile of each
      row; the tile is multiplied by 2 to that power before encoding.
 Values are rounded to bf16 (round to nearest even) or, for the fp8 cache,
@@ -210,9 +210,9 @@ def build_batch(rng: np.random.Generator, seq_lens, H: int, q_chunk: int,
         kv, scales = encode_e4m3_per_token(pool)
     elif kv_dtype == KV_FP8_LATENT:
         # 5. (this format only) every 128-column latent tile of every row is
-        # multiplied by 2^u, u uniform in [-3, 3], so that tile scales differ
-        # within a row and across rows
-        u = rng.integers(-3, 3, size=(num_pages, PAGE, 4), endpoint=True)
+        # multiplied by 2^u, u uniform in [-3, 0], so that tile scales differ
+        # within a row and across rows while values stay at the N(0,1) scale
+        u = rng.integers(-3, 0, size=(num_pages, PAGE, 4), endpoint=True)
         pool[..., :DIM_V] *= np.repeat(np.ldexp(np.float32(1.0), u).astype(np.float32), 128, axis=-1)
         kv = np.concatenate([encode_fp8_latent_rows(pool[i:i + 256]) for i in range(0, num_pages, 256)]) \
             if num_pages else np.zeros((0, PAGE, LATENT_ROW_BYTES), np.uint8)

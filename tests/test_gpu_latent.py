@@ -1,0 +1,102 @@
+"""GPU parity of the fp8 latent-row cache (SPLASH_KV_FP8_LATENT).
+
+A 656-byte row holds the 512 E4M3 latent codes, four fp32 tile scales (one
+per 128 latent columns) and the 64 RoPE values in bf16 (App. B, theoretical
+scenarios for DCU and H200, residency assumptions; the split and the scale
+granularity are this library's reading).  The oracle decodes the rows in
+float64; the kernel converts each latent tile with its scale for QK^T and
+scales each wave's P by its tile's key scales for PV.  The tolerances are
+the fp8 bar: outputs max-abs 3e-2, LSE 1e-3.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_37626_amd import binding as B
+from paper_2609_37626_amd import workloads as W
+from paper_2609_37626_amd.device import to_device
+from tests.test_gpu_parity import assert_parity, gpu_attend, run_oracle
+from tests.test_gpu_shards import check_merged, check_shards, page_cuts, run_shards
+
+pytestmark = pytest.mark.gpu
+
+LAT = W.KV_FP8_LATENT
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+CASES = {
+    # tails of every length class, a page-exact history, the longest here
+    "ragged_q1_H128": lambda: W.make_custom([1, 31, 32, 33, 63, 64, 65, 700, 2222, 5000], H=128, kv_dtype=LAT,
+                                            seed=61),
+    "chunk8_H128": lambda: W.make_custom([900, 1700, 2500], H=128, q_chunk=8, kv_dtype=LAT, seed=62),
+    "heads112_q1": lambda: W.make_custom([33, 640, 1999], H=112, kv_dtype=LAT, seed=63),
+    "heads16_q3": lambda: W.make_custom([50, 130, 3], H=16, q_chunk=3, kv_dtype=LAT, seed=64),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_latent_parity_against_oracle(name):
+    batch = CASES[name]()
+    print(f"{name}: lens {batch.seq_lens.tolist()} H={batch.H} q={batch.q_chunk}", flush=True)
+    out, lse = gpu_attend(batch)
+    assert_parity(batch, out, lse, label=name)
+
+
+@pytest.mark.parametrize("split_pages", [1, 3])
+def test_latent_forced_splits(split_pages):
+    batch = W.make_custom([3000, 77, 1500], H=128, kv_dtype=LAT, seed=65)
+    out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=split_pages)
+    assert_parity(batch, out, lse, label=f"latent split {split_pages}")
+
+
+def test_latent_poisoned_unused_rows_change_nothing():
+    clean = W.make_custom([63, 100, 129], H=128, q_chunk=2, kv_dtype=LAT, seed=66, extra_pages=2)
+    poisoned = W.poison_unused_rows(clean)
+    o1, l1 = gpu_attend(clean)
+    o2, l2 = gpu_attend(poisoned)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    assert_parity(clean, o1, l1, label="latent poison")
+
+
+def test_each_output_tile_takes_its_own_scale():
+    # every latent code 1.0 and tile scales 1/2, 2, 8, 1/8 in every row: the
+    # weights sum to one, so output columns [128t, 128t+128) equal scale t
+    batch = W.make_custom([300, 5, 64], H=128, kv_dtype=LAT, seed=67)
+    kv = batch.kv.copy()
+    kv[..., :512] = 0x38
+    kv[..., 512:528] = np.array([0.5, 2.0, 8.0, 0.125], dtype='<f4').view(np.uint8)
+    out, _ = gpu_attend(dataclasses.replace(batch, kv=kv))
+    o = out.float().cpu().numpy()
+    for t, sc in enumerate([0.5, 2.0, 8.0, 0.125]):
+        assert np.abs(o[..., 128 * t:128 * (t + 1)] - sc).max() <= 1e-2 * sc, t
+
+
+def test_latent_shards_merge_to_the_whole():
+    lens = np.random.Generator(np.random.PCG64(68)).integers(1, 3000, size=8, endpoint=True)
+    batch = W.make_custom(np.concatenate([lens, [1, 64, 65]]), H=128, kv_dtype=LAT, seed=68)
+    cuts = page_cuts(batch.seq_lens, 3, np.random.default_rng(68), empty_every=4)
+    part_out, part_lse, out, lse = run_shards(batch, cuts)
+    check_shards(batch, cuts, part_out, part_lse, "latent T=3")
+    check_merged(batch, out, lse, "latent T=3")
+
+
+def test_latent_debug_gather_is_bit_exact():
+    batch = W.make_custom([129, 7, 64], H=16, kv_dtype=LAT, seed=69)
+    db = to_device(batch)
+    total = int(batch.seq_lens.sum())
+    dense = torch.zeros((total, W.LATENT_ROW_BYTES), dtype=torch.uint8, device="cuda")
+    B.splash_mla_debug_gather(db.kv, db.block_table, db.seq_lens, db.desc(), dense)
+    torch.cuda.synchronize()
+    flat = batch.kv.reshape(batch.num_pages * 64, -1)
+    rows = [flat[int(batch.block_table[b, j // 64]) * 64 + j % 64]
+            for b, s in enumerate(batch.seq_lens) for j in range(int(s))]
+    assert np.array_equal(dense.cpu().numpy(), np.stack(rows))
+

@@ -97,6 +97,16 @@ def test_latent_rows_of_power_of_two_scales_are_bf16_exact():
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
 
 
+def test_latent_sampled_oracle_equals_batch_rows():
+    # the sampled oracle used at full size decodes the same rows
+    batch = W.make_custom([200, 70], H=16, kv_dtype=W.KV_FP8_LATENT, seed=70)
+    full, full_lse = oracle.mla_attention(batch.q, batch.kv, batch.block_table, batch.seq_lens, 1,
+                                          batch.softmax_scale, kv_dtype=2)
+    got, got_lse = oracle.mla_attention_sampled(batch.q, batch.kv, batch.block_table, batch.seq_lens, 1,
+                                                batch.softmax_scale, [(1, 0, 3), (0, 0, 15)], kv_dtype=2)
+    assert np.abs(got[0] - full[1, 3]).max() <= 1e-13 and abs(got_lse[1] - full_lse[0, 15]) <= 1e-13
+
+
 def test_single_key_returns_its_latent():
     assert pins.pin_single_key() == 0.0
 
