@@ -9,6 +9,7 @@ Default workload: many short requests (B=256, H=128, q=1, s ~ U[1024,4096],
 bf16 cache).  --config selects another of the five workloads.
 """
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -166,7 +167,7 @@ def run_topk(args, spec, batch):
         "data": "synthetic (seeded PCG64 draws of the workload's length mix; N(0,1) cache rows and queries; "
                 "uniform position choice)",
         "config": {"workload": spec.name, "B": batch.B, "H": H, "q_chunk": batch.q_chunk,
-                   "kv_cache": "fp8-e4m3+fp32 scale" if batch.kv_dtype else "bf16", "seed": spec.seed, "topk": K,
+                   "kv_cache": W.KV_LABELS[batch.kv_dtype], "seed": spec.seed, "topk": K,
                    "selected_rows": sel},
         "kv_gbps": round(sel * row_bytes / (ms * 1e-3) / 1e9, 1),
         "roofline": roof,
@@ -340,7 +341,7 @@ def run_sharded(args, spec, batch, db):
         "dtype": "bf16",
         "data": "synthetic (seeded PCG64 draws of the workload's length mix; N(0,1) cache rows and queries)",
         "config": {"workload": spec.name, "B": batch.B, "H": batch.H, "q_chunk": batch.q_chunk,
-                   "kv_cache": "fp8-e4m3+fp32 scale" if batch.kv_dtype else "bf16", "seed": spec.seed,
+                   "kv_cache": W.KV_LABELS[batch.kv_dtype], "seed": spec.seed,
                    "shards": N, "shard_cuts": "history b cut at floor(s_b k / N) rounded down to a page, k < N"},
         "phases_us": {"shards": [round(float(x) * 1e3, 2) for x in per_shard], "merge": round(merge_ms * 1e3, 2)},
         "roofline": roof,
@@ -371,6 +372,8 @@ def main():
                          "ranks (pack its head slice, assemble its own rows, and back)")
     ap.add_argument("--dop-rows", type=int, default=0,
                     help="with --dop-ranks: current query rows N (default: the workload's B * q_chunk)")
+    ap.add_argument("--kv-format", choices=["workload", "latent"], default="workload",
+                    help="latent: the workload's lengths over the fp8 latent-row cache (656-byte rows)")
     ap.add_argument("--shards", type=int, default=0,
                     help="position-sharded variant: cut every history into this many page-aligned shards, "
                          "run splash_mla_attend_shard per shard and splash_mla_combine over them")
@@ -392,7 +395,12 @@ def main():
     assert torch.cuda.is_available(), "bench needs a GPU"
     spec = W.CONFIGS[args.config]
     t0 = time.perf_counter()
-    batch = W.make_config(args.config)
+    if args.kv_format == "latent":
+        batch = W.make_config(args.config, kv_dtype=W.KV_FP8_LATENT)
+        spec = dataclasses.replace(spec, name=spec.name.replace(" e4m3", "") + " fp8-latent-rows",
+                                   kv_dtype=W.KV_FP8_LATENT)
+    else:
+        batch = W.make_config(args.config)
     log(f"workload {spec.name}: generated in {time.perf_counter() - t0:.1f} s")
     if args.dop_ranks > 0:
         return run_dop(args, spec, batch)
@@ -512,7 +520,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded PCG64 draws of the workload's length mix; N(0,1) cache rows and queries)",
         "config": {"workload": spec.name, "B": batch.B, "H": batch.H, "q_chunk": batch.q_chunk,
-                   "lengths": list(spec.lengths), "kv_cache": "fp8-e4m3+fp32 scale" if batch.kv_dtype else "bf16",
+                   "lengths": list(spec.lengths), "kv_cache": W.KV_LABELS[batch.kv_dtype],
                    "seed": spec.seed, "sum_seq_len": int(batch.seq_lens.sum()), "page_size": 64},
         "kv_gbps": round(kv_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "alg_gbps": round(alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),

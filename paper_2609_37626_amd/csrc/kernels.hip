@@ -26,6 +26,10 @@
 //    accumulation registers per lane.
 //  * fp8 cache: E4M3 codes convert exactly to bf16; the per-token scale is
 //    applied in fp32 to the score and to P before P is rounded for PV.
+//  * fp8 latent-row cache (656-byte rows: E4M3 latent with a power-of-two
+//    scale per 128 columns, bf16 RoPE): K tiles convert with their scale;
+//    for PV, wave w's output columns are tile w, so its P weights take the
+//    keys' tile-w scales.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>

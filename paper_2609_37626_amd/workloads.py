@@ -232,12 +232,19 @@ def build_batch(rng: np.random.Generator, seq_lens, H: int, q_chunk: int,
                  H=H, kv_dtype=kv_dtype, softmax_scale=SOFTMAX_SCALE)
 
 
-def make_config(cfg: int, seed: Optional[int] = None, unused_slot: int = -1) -> Batch:
-    """Batch of workload ``cfg`` (1..5); seed defaults to ``cfg - 1``."""
+def make_config(cfg: int, seed: Optional[int] = None, unused_slot: int = -1,
+                kv_dtype: Optional[int] = None) -> Batch:
+    """Batch of workload ``cfg`` (1..5); seed defaults to ``cfg - 1``;
+    ``kv_dtype`` overrides the workload's cache format (same lengths)."""
     spec = CONFIGS[cfg]
     rng = np.random.Generator(np.random.PCG64(spec.seed if seed is None else seed))
     seq_lens = draw_lengths(rng, spec)
-    return build_batch(rng, seq_lens, spec.H, spec.q_chunk, spec.kv_dtype, unused_slot)
+    return build_batch(rng, seq_lens, spec.H, spec.q_chunk, spec.kv_dtype if kv_dtype is None else kv_dtype,
+                       unused_slot)
+
+
+KV_LABELS = {KV_BF16: "bf16", KV_FP8_E4M3: "fp8-e4m3+fp32 scale",
+             KV_FP8_LATENT: "fp8-e4m3 latent, fp32 tile scales, bf16 rope (656 B rows)"}
 
 
 def make_custom(seq_lens, H: int, q_chunk: int = 1, kv_dtype: int = KV_BF16,
