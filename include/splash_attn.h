@@ -70,8 +70,10 @@ extern "C" {
  * [num_pages, 64, 656] bytes; a row is 512 OCP E4M3 latent codes, four
  * little-endian fp32 scales (scale t covers latent columns [128t, 128t+128))
  * and the 64 RoPE values as bf16: K[d] = e4m3(code[d]) * scale[d / 128] for
- * d < 512, K[512 + r] = rope[r].  Scales must be powers of two (finite,
- * nonzero; NaN rows only where no history reaches); kv_scales is ignored.
+ * d < 512, K[512 + r] = rope[r].  Scales must be positive normal powers
+ * of two (the conversion uses only a scale's exponent); rows no history
+ * reaches may hold anything.  SPLASH_FLAG_DEBUG_CHECK rejects a reached
+ * row whose scale is not.  kv_scales is ignored.
  * splash_mla_attend, splash_mla_attend_shard and the gather take it; the
  * top-k variant returns SPLASH_ERR_UNSUPPORTED. */
 #define SPLASH_KV_FP8_LATENT 2

@@ -165,10 +165,11 @@ struct Shard {
   int32_t topk = 0;
 };
 
-int check_device_data(const int32_t* block_table, const int32_t* seq_lens, int32_t q_chunk,
+int check_device_data(const void* kv_pages, const int32_t* block_table, const int32_t* seq_lens, int32_t q_chunk,
                       const splash_mla_desc* d, const Workspace& wv, hipStream_t s, const Shard& sh = Shard()) {
   int32_t* res = wv.header + kHdrDebug;
-  hipError_t e = launch_check(block_table, seq_lens, sh.key_begin, sh.key_end, d->batch, q_chunk,
+  const void* latent_kv = d->kv_dtype == SPLASH_KV_FP8_LATENT ? kv_pages : nullptr;
+  hipError_t e = launch_check(block_table, seq_lens, latent_kv, sh.key_begin, sh.key_end, d->batch, q_chunk,
                               d->max_pages_per_seq, d->num_pages, res, s);
   if (e != hipSuccess) return hip_fail(e, "check launch");
   int32_t host = 0;
@@ -178,8 +179,8 @@ int check_device_data(const int32_t* block_table, const int32_t* seq_lens, int32
   if (host != INT32_MAX)
     return fail(SPLASH_ERR_INVALID_ARGUMENT,
                 "request %d: seq_len < q_chunk, history longer than the block-table row, a block-table "
-                "entry outside [0, num_pages), or (shard) a key range that is not 0 <= begin <= end with begin "
-                "a multiple of 64",
+                "entry outside [0, num_pages), (shard) a key range that is not 0 <= begin <= end with begin "
+                "a multiple of 64, or (latent-row cache) a tile scale that is not a positive power of two",
                 host - 1);
   return SPLASH_OK;
 }
@@ -342,7 +343,7 @@ int splash_mla_run(const void* q, const void* kv_pages, const int32_t* block_tab
   if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
-    if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
+    if ((st = check_device_data(kv_pages, block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
 }
 
@@ -386,7 +387,7 @@ int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_
   if ((st = prepare(seq_lens, q_chunk, desc, workspace, ws_bytes, &wv)) != SPLASH_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
-    if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
+    if ((st = check_device_data(kv_pages, block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   if ((st = do_plan(seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
 }
@@ -468,7 +469,7 @@ int splash_mla_attend_shard(const void* q, const void* kv_pages, const int32_t* 
   sh.num_shards = num_shards;
   sh.shard = shard;
   if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
-    if ((st = check_device_data(block_table, seq_lens, q_chunk, desc, wv, s, sh)) != SPLASH_OK) return st;
+    if ((st = check_device_data(kv_pages, block_table, seq_lens, q_chunk, desc, wv, s, sh)) != SPLASH_OK) return st;
   if ((st = do_plan(seq_lens, q_chunk, desc, wv, s, sh)) != SPLASH_OK) return st;
   if ((st = do_attend_units(q, kv_pages, block_table, seq_lens, q_chunk, part_out, part_lse, desc, wv, s, sh)) !=
       SPLASH_OK)

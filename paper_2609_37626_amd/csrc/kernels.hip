@@ -1715,10 +1715,13 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint8_t* kv, const in
 // entry in [0, num_pages); under a shard also 0 <= key_begin[b] <= key_end[b]
 // with key_begin[b] a page boundary, and only the shard's pages are used.
 // Writes the smallest failing request + 1 (or 0).
+// latent_kv (the fp8 latent-row pool, else null): once every page entry of a
+// request is in range, each of its rows' four tile scales must be a positive
+// normal power of two.
 __global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int32_t* seq_lens,
                                                     const int32_t* key_begin, const int32_t* key_end, int32_t B,
                                                     int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
-                                                    int32_t* result) {
+                                                    const uint8_t* latent_kv, int32_t* result) {
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
     const int s = seq_lens[b];
     bool bad = s < q_chunk || (int64_t)(s + kPage - 1) / kPage > bt_stride;
@@ -1733,6 +1736,17 @@ __global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int
       for (int k = lo / kPage + threadIdx.x; k < np; k += blockDim.x) {
         const int v = bt[(size_t)b * bt_stride + k];
         if (v < 0 || v >= num_pages) bad = true;
+      }
+    }
+    if (latent_kv && !__syncthreads_or(bad) && hi > lo) {
+      for (int j = lo + threadIdx.x; j < hi; j += blockDim.x) {
+        const size_t row = (size_t)bt[(size_t)b * bt_stride + (j >> 6)] * kPage + (j & (kPage - 1));
+        const u32x4 sc = *(const u32x4*)(latent_kv + row * kLatentRowBytes + 512);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const uint32_t e = (sc[t] >> 23) & 0xFF;
+          if ((sc[t] & 0x807FFFFFu) != 0 || e == 0 || e == 0xFF) bad = true;
+        }
       }
     }
     if (bad) atomicMin(result, b + 1);
@@ -1820,13 +1834,13 @@ hipError_t launch_topk_check(const int32_t* bt, const int32_t* seq_lens, const i
   return hipGetLastError();
 }
 
-hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* key_begin,
+hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, const void* latent_kv, const int32_t* key_begin,
                         const int32_t* key_end, int32_t B, int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
                         int32_t* result, hipStream_t s) {
   hipLaunchKernelGGL(init_check, dim3(1), dim3(1), 0, s, result);
   int blocks = B < 1024 ? B : 1024;
   hipLaunchKernelGGL(check_kernel, dim3(blocks), dim3(256), 0, s, bt, seq_lens, key_begin, key_end, B, q_chunk,
-                     bt_stride, num_pages, result);
+                     bt_stride, num_pages, (const uint8_t*)latent_kv, result);
   return hipGetLastError();
 }
 

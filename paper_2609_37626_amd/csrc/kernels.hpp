@@ -95,7 +95,7 @@ hipError_t launch_dop_unpack_q(const void* recv, int32_t T, int32_t n, int32_t h
 hipError_t launch_dop_pack_out(const void* out_owner, int32_t T, int32_t n, int32_t hl, void* send, hipStream_t s);
 hipError_t launch_dop_unpack_out(const void* recv, const int32_t* order, int32_t n, int32_t hl, void* out,
                                  hipStream_t s);
-hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* key_begin,
+hipError_t launch_check(const int32_t* bt, const int32_t* seq_lens, const void* latent_kv, const int32_t* key_begin,
                         const int32_t* key_end, int32_t B, int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
                         int32_t* result, hipStream_t s);
 

@@ -100,3 +100,21 @@ def test_latent_debug_gather_is_bit_exact():
             for b, s in enumerate(batch.seq_lens) for j in range(int(s))]
     assert np.array_equal(dense.cpu().numpy(), np.stack(rows))
 
+
+
+def test_debug_check_rejects_scales_that_are_not_powers_of_two():
+    batch = W.make_custom([130, 64], H=16, kv_dtype=LAT, seed=71)
+    out_ref, lse_ref = gpu_attend(batch)
+    out_dbg, lse_dbg = gpu_attend(batch, flags=B.FLAG_DEBUG_CHECK)   # valid data passes, same result
+    assert torch.equal(out_ref.view(torch.int16), out_dbg.view(torch.int16)) and torch.equal(lse_ref, lse_dbg)
+    p0, p1 = int(batch.block_table[0, 2]), int(batch.block_table[1, 0])
+    for page, row, value in [(p0, 1, 3.0), (p1, 63, -0.5), (p0, 0, 0.0), (p0, 1, np.inf)]:
+        kv = batch.kv.copy()
+        kv[page, row, 512 + 4:512 + 8] = np.array([value], dtype='<f4').view(np.uint8)   # tile 1
+        with pytest.raises(B.SplashError):
+            gpu_attend(dataclasses.replace(batch, kv=kv), flags=B.FLAG_DEBUG_CHECK)
+    # a row past the end of history 0 (130 keys: page 2 holds keys 128, 129)
+    # is never reached, so its scales may hold anything
+    kv = batch.kv.copy()
+    kv[p0, 5, 512:528] = np.full(4, 3.0, dtype='<f4').view(np.uint8)
+    gpu_attend(dataclasses.replace(batch, kv=kv), flags=B.FLAG_DEBUG_CHECK)
