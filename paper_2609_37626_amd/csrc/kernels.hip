@@ -563,13 +563,15 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
 // Latent rows (LAT: 656 B = 512 E4M3 codes at 0 | 4 fp32 tile scales at 512
 // | 64 bf16 RoPE at 528): in LDS the latent's 8 line groups as fp8, then the
 // RoPE as one bf16 line group at kRopeOff, then the rows' tile scales (16 B
-// per row) at kData.
+// per row) at kData, and at kScaleT the same scales tile-major ([tile][row],
+// written by wave 0 once its loads landed).
 template <bool FP8, bool LAT = false>
 struct StepLayout {
   static constexpr int kRowBytes = LAT ? 656 : FP8 ? kDimQK : 2 * kDimQK;   // 656 / 576 / 1152
   static constexpr int kRopeOff = 8 * kStepKeys * 64;                      // LAT: 16384
   static constexpr int kData = LAT ? kRopeOff + kStepKeys * 128 : kStepKeys * kRowBytes;  // 20480 / 18432 / 36864
-  static constexpr int kBuf = LAT ? kData + 1024 : FP8 ? kData + 256 : kData;             // + fp32 scales
+  static constexpr int kScaleT = kData + 1024;                                            // LAT
+  static constexpr int kBuf = LAT ? kData + 1536 : FP8 ? kData + 256 : kData;             // + fp32 scales
   // Ring slots: the step being multiplied (QK), the previous one (PV), and
   // kDist steps in flight.
   static constexpr int kSlots = FP8 ? 4 : 3;
@@ -816,11 +818,17 @@ __device__ __forceinline__ bf16x8 scale_p(bf16x8 p, const float (&s)[8]) {
 
 // Latent rows: the tile-`wave` scales of the 8 keys of the P^T fragment
 // (key half kh) a lane reads; element e is key 16kh + 8(e >> 2) + 4h + (e & 3)
-// (the slot order of the P exchange).
-__device__ __forceinline__ void load_p_scales(const uint8_t LDS_AS* scales, int kh, int h, int wave, float (&s)[8]) {
+// (the slot order of the P exchange).  scales_t: the tile-major copy, so the
+// two runs of 4 keys are two 16-byte reads.
+__device__ __forceinline__ void load_p_scales(const uint8_t LDS_AS* scales_t, int kh, int h, int wave,
+                                              float (&s)[8]) {
+  const uint8_t LDS_AS* base = scales_t + 4 * (32 * wave + 16 * kh + 4 * h);
+  const f32x4 a = *(const f32x4 LDS_AS*)base, b = *(const f32x4 LDS_AS*)(base + 32);
 #pragma unroll
-  for (int e = 0; e < 8; ++e)
-    s[e] = *(const float LDS_AS*)(scales + 16 * (16 * kh + 8 * (e >> 2) + 4 * h + (e & 3)) + 4 * wave);
+  for (int e = 0; e < 4; ++e) {
+    s[e] = a[e];
+    s[4 + e] = b[e];
+  }
 }
 
 // P^T operand fragment (head block hb, key half kh) from the P exchange area:
@@ -832,8 +840,8 @@ __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t ha
 // PV of one 32-key step as a standalone MFMA stream (the unit's last step,
 // which has no QK to interleave with): 32 MFMAs,
 // o[cbl][hb] += V^T(cb = 4*wave + cbl, kh) P^T(hb, kh) with V from `vbuf` and
-// P from the P exchange area (LAT: P scaled by the keys' tile scales, which
-// sit at vbuf + lat_scales).
+// P from the P exchange area (LAT: P scaled by the keys' tile scales, whose
+// tile-major copy sits at vbuf + lat_scales).
 template <bool FP8, bool LAT = false>
 __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint32_t (*vbase)[2],
                                           const uint8_t LDS_AS* p_lds, int wave, int n32, int h,
@@ -1137,6 +1145,14 @@ void attend_kernel(AttendLaunch a) {
             if (wave >= 2 && (int)(lane & 31) >= valid) *(float LDS_AS*)(buf + L::kData + 4 * lane) = 0.f;
           }
         }
+        if constexpr (LAT) {
+          // the tile-major copy of the step's scales (after the zero fill)
+          if (wave == 0 && lane < 32) {
+            const f32x4 v = *(const f32x4 LDS_AS*)(buf + L::kData + 16 * lane);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) *(float LDS_AS*)(buf + L::kScaleT + 4 * (32 * t + lane)) = v[t];
+          }
+        }
         // step j staged; P of step j-1 visible; every wave is done with
         // iteration j-1, so the slot of step j-2 is free
         lds_barrier();
@@ -1162,10 +1178,7 @@ void attend_kernel(AttendLaunch a) {
 #pragma unroll
           for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_raw<FP8>(buf, kbase, ks);
           if constexpr (kPV) {
-            if constexpr (LAT) {
-              load_p_scales(vbuf + L::kData, 0, h, wave, psc[0]);
-              load_p_scales(vbuf + L::kData, 1, h, wave, psc[1]);
-            }
+            if constexpr (LAT) load_p_scales(vbuf + L::kScaleT, 0, h, wave, psc[0]);
 #pragma unroll
             for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 0, h));
             vf[0] = load_v_raw<FP8>(vbuf, vbase, 4 * wave, 0);
@@ -1202,9 +1215,9 @@ void attend_kernel(AttendLaunch a) {
             if (q != kNone) {
               const int c = q >> 2, hb = q & 3;
               if constexpr (LAT) {
-                // P scaled at its first use (its 4 column blocks share it)
+                // P scaled at its first use (its 4 column blocks share it;
+                // those of key half 1 are scaled in stream 2)
                 if (c == 0) pf[hb] = scale_p(pf[hb], psc[0]);
-                if (c == 4) pf1[hb] = scale_p(pf1[hb], psc[1]);
               }
               const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
               if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
@@ -1260,8 +1273,13 @@ void attend_kernel(AttendLaunch a) {
             if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
             o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
             // (as in stream 1) the key half 1 P fragment after the last read
-            // of the half 0 one
-            if (c == 3) pf1[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
+            // of the half 0 one (LAT: with its key scales)
+            if (c == 3) {
+              pf1[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 1, h));
+              if constexpr (LAT) {
+                if (hb == 0) load_p_scales(vbuf + L::kScaleT, 1, h, wave, psc[1]);
+              }
+            }
           }
         };
         // kLead PV MFMAs run while the QK chain drains, the last kTail after
@@ -1386,7 +1404,8 @@ void attend_kernel(AttendLaunch a) {
       for (int j = 1; j < nsteps; ++j) qk_softmax(j, std::true_type{});
       // PV of the last step
       lds_barrier();
-      pv_stream<FP8, LAT>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o, L::kData);
+      pv_stream<FP8, LAT>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o,
+                          L::kScaleT);
       const float mt_max = fmaxf(tmax, wave_xor32(tmax));
       const float m_seen = m_ref + mt_max;
       const bool over = mt_max > 64.0f;
