@@ -395,6 +395,9 @@ def main():
     assert torch.cuda.is_available(), "bench needs a GPU"
     spec = W.CONFIGS[args.config]
     t0 = time.perf_counter()
+    if args.kv_format == "latent" and (args.topk > 0 or args.dop_ranks > 0):
+        print("--kv-format latent runs the dense and sharded attention only", file=sys.stderr)
+        sys.exit(2)
     if args.kv_format == "latent":
         batch = W.make_config(args.config, kv_dtype=W.KV_FP8_LATENT)
         spec = dataclasses.replace(spec, name=spec.name.replace(" e4m3", "") + " fp8-latent-rows",

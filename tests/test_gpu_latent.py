@@ -118,3 +118,11 @@ def test_debug_check_rejects_scales_that_are_not_powers_of_two():
     kv = batch.kv.copy()
     kv[p0, 5, 512:528] = np.full(4, 3.0, dtype='<f4').view(np.uint8)
     gpu_attend(dataclasses.replace(batch, kv=kv), flags=B.FLAG_DEBUG_CHECK)
+
+
+def test_latent_history_longer_than_one_unit():
+    # 70,000 keys = 1,094 pages: more than one unit may hold, so the history
+    # is split and its partials combined
+    batch = W.make_custom([70000, 3000], H=32, kv_dtype=LAT, seed=72)
+    out, lse = gpu_attend(batch)
+    assert_parity(batch, out, lse, label="latent 70000 keys")

@@ -94,3 +94,25 @@ def test_workload_accounting_cfg2():
     assert kv == 661514 * 1152
     assert flops == 2 * 128 * 1088 * 661514
     assert 833e6 < total < 834e6
+
+
+def test_latent_rows_recipe():
+    # 656-byte rows: every tile scale is the smallest power of two not below
+    # max|tile| / 448 (so max|tile| / scale lies in (224, 448], and its E4M3
+    # code in [224, 448]: the codes are 32 apart there), codes are
+    # finite, the RoPE bytes are the bf16 rounding of the drawn values, and
+    # the other draws of the stream are those of the bf16 cache
+    b = W.make_custom([70, 130, 64], H=16, q_chunk=2, kv_dtype=W.KV_FP8_LATENT, seed=9)
+    assert b.kv.shape == (b.num_pages, 64, 656) and b.kv.dtype == np.uint8
+    rows = b.kv.reshape(-1, 656)
+    scales = rows[:, 512:528].copy().view('<f4')
+    m, e = np.frexp(scales)
+    assert np.all(m == 0.5)                                    # powers of two
+    codes = torch.from_numpy(rows[:, :512].copy()).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.all(np.isfinite(codes))
+    amax = np.abs(codes.reshape(-1, 4, 128)).max(axis=-1)
+    assert np.all((amax >= 224) & (amax <= 448))
+    assert len(np.unique(scales)) >= 3                         # tile scales differ
+    ref = W.make_custom([70, 130, 64], H=16, q_chunk=2, kv_dtype=W.KV_BF16, seed=9)
+    assert np.array_equal(b.q, ref.q) and np.array_equal(b.block_table, ref.block_table)
+    assert np.array_equal(rows[:, 528:].copy().view('<u2'), ref.kv.reshape(-1, 576)[:, 512:])
