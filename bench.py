@@ -97,6 +97,7 @@ def run_topk(args, spec, batch):
     import torch
 
     from paper_2609_37626_amd import binding as B
+    from paper_2609_37626_amd import workloads as W
     from paper_2609_37626_amd.device import to_device
 
     K = args.topk
@@ -143,7 +144,7 @@ def run_topk(args, spec, batch):
     call_us = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
 
     sel = int(cnt.sum())
-    row_bytes = 580 if batch.kv_dtype else 1152
+    row_bytes = {W.KV_BF16: 1152, W.KV_FP8_E4M3: 580, W.KV_FP8_LATENT: W.LATENT_ROW_BYTES}[batch.kv_dtype]
     H = batch.H
     alg_bytes = sel * row_bytes + N * H * (576 * 2 + 512 * 2 + 4) + sel * 4
     flops = 2.0 * H * (576 + 512) * sel
@@ -395,8 +396,8 @@ def main():
     assert torch.cuda.is_available(), "bench needs a GPU"
     spec = W.CONFIGS[args.config]
     t0 = time.perf_counter()
-    if args.kv_format == "latent" and (args.topk > 0 or args.dop_ranks > 0):
-        print("--kv-format latent runs the dense and sharded attention only", file=sys.stderr)
+    if args.kv_format == "latent" and args.dop_ranks > 0:
+        print("--kv-format latent applies to the attention modes, not the DOP regroup", file=sys.stderr)
         sys.exit(2)
     if args.kv_format == "latent":
         batch = W.make_config(args.config, kv_dtype=W.KV_FP8_LATENT)

@@ -74,8 +74,8 @@ extern "C" {
  * of two (the conversion uses only a scale's exponent); rows no history
  * reaches may hold anything.  SPLASH_FLAG_DEBUG_CHECK rejects a reached
  * row whose scale is not.  kv_scales is ignored.
- * splash_mla_attend, splash_mla_attend_shard and the gather take it; the
- * top-k variant returns SPLASH_ERR_UNSUPPORTED. */
+ * Every attend entry point (whole histories, shards, top-k) and the gather
+ * take it. */
 #define SPLASH_KV_FP8_LATENT 2
 
 /* ---- flags ------------------------------------------------------------------ */

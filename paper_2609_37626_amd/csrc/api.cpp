@@ -398,8 +398,6 @@ int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* b
                            const splash_mla_desc* desc, void* workspace, size_t ws_bytes, void* stream) {
   int st = validate_desc(desc, q_chunk);
   if (st != SPLASH_OK) return st;
-  if (desc->kv_dtype == SPLASH_KV_FP8_LATENT)
-    return fail(SPLASH_ERR_UNSUPPORTED, "the top-k variant reads bf16 or per-token fp8 caches");
   if (desc->batch == 0) return SPLASH_OK;
   if (!topk_idx || !topk_count) return fail(SPLASH_ERR_INVALID_ARGUMENT, "topk_idx and topk_count must be non-NULL");
   if (topk < 1 || topk > (1 << 24)) return fail(SPLASH_ERR_INVALID_ARGUMENT, "topk must be in [1, 2^24] (got %d)", topk);

@@ -675,10 +675,30 @@ __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, 
 
 // Top-k variant: the lane's row of the step is a gathered pool row, at
 // row_addr (its chunk included); its token scale (fp8, waves 2 and 3) at
-// scale_addr.  Same LDS placement as issue_one.
-template <bool FP8, int t>
-__device__ __forceinline__ void issue_one_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave) {
-  if constexpr (!FP8) {
+// scale_addr.  Same LDS placement as issue_one.  LAT: the RoPE and tile-scale
+// loads take other rows of the step than the latent ones; their pool rows
+// are read here from step_rows (the step's 32 resolved rows in LDS), their
+// bytes from the pool at kv.
+template <bool FP8, int t, bool LAT = false>
+__device__ __forceinline__ void issue_one_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave,
+                                            const int32_t LDS_AS* step_rows, const uint8_t* kv) {
+  if constexpr (LAT) {
+    using L = StepLayout<true, true>;
+    if constexpr (t < 4) {
+      dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+    } else {
+      uint32_t ln;
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+      const uint64_t base = (uint64_t)(uintptr_t)kv;
+      if constexpr (t == 4) {
+        const uint32_t r = 8 * wave + (ln >> 3);
+        dma_b128_v(base + (uint64_t)(uint32_t)step_rows[r] * L::kRowBytes + 528 + (((ln & 7) ^ ((r >> 1) & 7)) * 16),
+                   buf + L::kRopeOff + 1024 * wave);
+      } else if (wave == 0) {
+        dma_b128_v(base + (uint64_t)(uint32_t)step_rows[ln & 31] * L::kRowBytes + 512, buf + L::kData);
+      }
+    }
+  } else if constexpr (!FP8) {
     dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 1024 * wave);
   } else {
     if (t < 4 || wave + 4 * t < 18)
@@ -687,11 +707,12 @@ __device__ __forceinline__ void issue_one_v(uint64_t row_addr, uint64_t scale_ad
       dma_b32_v(scale_addr, buf + 18432);
   }
 }
-template <bool FP8, int t = 0>
-__device__ __forceinline__ void issue_from_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave) {
-  if constexpr (t < StepLayout<FP8>::kLoadsPerStep) {
-    issue_one_v<FP8, t>(row_addr, scale_addr, buf, wave);
-    issue_from_v<FP8, t + 1>(row_addr, scale_addr, buf, wave);
+template <bool FP8, bool LAT, int t = 0>
+__device__ __forceinline__ void issue_from_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave,
+                                             const int32_t LDS_AS* step_rows, const uint8_t* kv) {
+  if constexpr (t < StepLayout<FP8, LAT>::kLoadsPerStep) {
+    issue_one_v<FP8, t, LAT>(row_addr, scale_addr, buf, wave, step_rows, kv);
+    issue_from_v<FP8, LAT, t + 1>(row_addr, scale_addr, buf, wave, step_rows, kv);
   }
 }
 
@@ -888,7 +909,7 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
 template <bool FP8, bool TOPK, bool LAT = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
-  static_assert(!LAT || (FP8 && !TOPK), "latent rows: dense fp8 variant only");
+  static_assert(!LAT || FP8, "latent rows are an fp8 variant");
   using L = StepLayout<FP8, LAT>;
   constexpr int kPOff = L::kRing;                    // P exchange area, two steps
   constexpr int kLOff = kPOff + 2 * kPBytes;         // per-head normaliser, 128 floats
@@ -1072,7 +1093,8 @@ void attend_kernel(AttendLaunch a) {
       for (int j = 0; j < L::kDist; ++j)
         if (j < nsteps) {
           if constexpr (TOPK) {
-            issue_from_v<FP8>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave);
+            issue_from_v<FP8, LAT>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave,
+                                   s_bt + j * kStepKeys, kv);
           } else {
             const int ph = step_phys(j);
             issue_step<FP8, LAT>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
@@ -1112,6 +1134,7 @@ void attend_kernel(AttendLaunch a) {
         const uint8_t* pf_src = step_src(j + L::kDist, pf_phys);
         const float* pf_scales = step_scales(j + L::kDist, pf_phys);
         uint64_t pf_row = 0, pf_srow = 0;
+        const int32_t LDS_AS* pf_rows = s_bt + (j + L::kDist) * kStepKeys;  // top-k: rows of step j + kDist
         if constexpr (TOPK) {
           pf_row = row_addr(j == 0 ? next_row : next_row_v);
           pf_srow = scale_addr(j == 0 ? next_srow : next_srow_v);
@@ -1230,15 +1253,15 @@ void attend_kernel(AttendLaunch a) {
             if ((i & 3) == 1 && (i >> 2) < L::kLoadsPerStep && pf_next) {
               if constexpr (TOPK) {
                 switch (i >> 2) {
-                  case 0: issue_one_v<FP8, 0>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 1: issue_one_v<FP8, 1>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 2: issue_one_v<FP8, 2>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 3: issue_one_v<FP8, 3>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 4: issue_one_v<FP8, 4>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 5: issue_one_v<FP8, 5>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 6: issue_one_v<FP8, 6>(pf_row, pf_srow, pf_buf, wave); break;
-                  case 7: issue_one_v<FP8, 7>(pf_row, pf_srow, pf_buf, wave); break;
-                  default: issue_one_v<FP8, 8>(pf_row, pf_srow, pf_buf, wave); break;
+                  case 0: issue_one_v<FP8, 0, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 1: issue_one_v<FP8, 1, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 2: issue_one_v<FP8, 2, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 3: issue_one_v<FP8, 3, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 4: issue_one_v<FP8, 4, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 5: issue_one_v<FP8, 5, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 6: issue_one_v<FP8, 6, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 7: issue_one_v<FP8, 7, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  default: issue_one_v<FP8, 8, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
                 }
               } else {
                 switch (i >> 2) {
@@ -1810,7 +1833,11 @@ hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
 
 hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) {
   if (a.kv_dtype == 2) {
-    hipLaunchKernelGGL((attend_kernel<true, false, true>), dim3(workers), dim3(256), 0, s, a);
+    if (a.topk_idx) {
+      hipLaunchKernelGGL((attend_kernel<true, true, true>), dim3(workers), dim3(256), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((attend_kernel<true, false, true>), dim3(workers), dim3(256), 0, s, a);
+    }
   } else if (a.kv_dtype == 1) {
     if (a.topk_idx) {
       hipLaunchKernelGGL((attend_kernel<true, true>), dim3(workers), dim3(256), 0, s, a);

@@ -107,17 +107,13 @@ def test_idle_owner_is_a_noop_even_with_null_pointers():
     assert L.splash_mla_combine(None, None, None, 0, 1, 16, None, None, None) == B.SPLASH_OK
 
 
-def test_latent_row_cache_is_accepted_without_scales_and_refused_by_top_k():
-    # the latent-row cache carries its scales in the rows: no kv_scales, and
-    # an idle owner returns OK; the top-k variant does not take this format
+def test_latent_row_cache_is_accepted_without_scales():
+    # the latent-row cache carries its scales in the rows: no kv_scales; an
+    # idle owner returns OK through the dense and the top-k entry points
     assert call_attend(good_desc(kv_dtype=B.KV_FP8_LATENT, batch=0), q=0, kv=0, bt=0, seq=0, out=0, lse=0,
                        ws=0, ws_bytes=0) == B.SPLASH_OK
-    L = B.lib()
-    d = good_desc(kv_dtype=B.KV_FP8_LATENT)
-    st = L.splash_mla_attend_topk(FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, 64, FAKE, FAKE, ctypes.byref(d), FAKE,
-                                  1 << 30, None)
-    assert st == B.SPLASH_ERR_UNSUPPORTED
-    assert b"top-k" in B.lib().splash_last_error()
+    d = good_desc(kv_dtype=B.KV_FP8_LATENT, batch=0)
+    assert B.lib().splash_mla_attend_topk(0, 0, 0, 0, 1, 0, 0, 64, 0, 0, ctypes.byref(d), 0, 0, None) == B.SPLASH_OK
 
 
 def call_shard(desc, kb=FAKE, ke=FAKE, num_shards=2, shard=0, part_out=FAKE, part_lse=FAKE, ws_bytes=1 << 30):

@@ -126,3 +126,16 @@ def test_latent_history_longer_than_one_unit():
     batch = W.make_custom([70000, 3000], H=32, kv_dtype=LAT, seed=72)
     out, lse = gpu_attend(batch)
     assert_parity(batch, out, lse, label="latent 70000 keys")
+
+
+@pytest.mark.parametrize("k,q_chunk", [(64, 1), (700, 1), (3000, 1), (300, 8)])
+def test_latent_topk_against_oracle(k, q_chunk):
+    # top-k rows over latent rows: the sparse attention of the paper's
+    # backend over the DeepSeek-V3.2-style cache (k = 3000 splits a list
+    # over units)
+    from tests.test_gpu_topk import check, lists, run_topk
+    lens = np.random.Generator(np.random.PCG64(73 + k)).integers(q_chunk, 4000, size=6, endpoint=True)
+    batch = W.make_custom(lens, H=128, q_chunk=q_chunk, kv_dtype=LAT, seed=73)
+    idx, cnt = lists(batch, k, np.random.default_rng(k), empty_rows=(1,), recent=8)
+    out, lse = run_topk(batch, idx, cnt)
+    check(batch, idx, cnt, out, lse, f"latent top-k k={k} q={q_chunk}")
