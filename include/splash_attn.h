@@ -72,8 +72,9 @@ extern "C" {
  * and the 64 RoPE values as bf16: K[d] = e4m3(code[d]) * scale[d / 128] for
  * d < 512, K[512 + r] = rope[r].  Scales must be positive normal powers
  * of two (the conversion uses only a scale's exponent); rows no history
- * reaches may hold anything.  SPLASH_FLAG_DEBUG_CHECK rejects a reached
- * row whose scale is not.  kv_scales is ignored.
+ * reaches may hold anything.  Under SPLASH_FLAG_DEBUG_CHECK the whole-history
+ * and shard entry points reject a reached row whose scale is not (the top-k
+ * check validates lists and pages only).  kv_scales is ignored.
  * Every attend entry point (whole histories, shards, top-k) and the gather
  * take it. */
 #define SPLASH_KV_FP8_LATENT 2
