@@ -6,24 +6,32 @@
 //  * Work unit = (query row n with all H heads, page range).  Under a fold
 //    plan each worker runs its own run of units; otherwise units come from a
 //    device queue filled by the planner, drawn with one atomic.
-//  * 4 waves; wave w owns heads [32w, 32w+32).  Its 32 query rows stay in
-//    VGPRs for the whole unit (36 x 16-byte MFMA B fragments).
+//  * 4 waves, one per SIMD.  For QK^T and the softmax wave w owns heads
+//    [32w, 32w+32), whose query rows stay in VGPRs for the whole unit (36
+//    16-byte MFMA B fragments); for PV it owns output columns [128w, +128)
+//    of all heads, 256 accumulation registers per lane.
 //  * KV is staged 32 rows (half a page, one "step") at a time straight from
-//    HBM into LDS with 16-byte direct-to-LDS loads, 3 steps in flight in a
-//    4-deep ring.  The chunk order of each row is XOR-permuted by row so the
-//    operand reads below spread over the LDS banks.
-//  * S^T[32 keys x 32 heads] = K Q^T on v_mfma_f32_32x32x16_bf16 (36 MFMAs),
-//    K read from LDS as the A operand.  In that C layout a lane holds one head
-//    and 16 keys, so the row max needs one cross-half exchange.
-//  * Online softmax in base 2 with lazy rescaling: the running max only moves
-//    (and O is only rescaled) when the new max exceeds it by more than 8, so
-//    P <= 2^8; the result is exact because numerator and denominator share
-//    the same reference max.
-//  * O^T[512 x 32 heads] += V^T P^T on MFMA: P^T comes straight from the S^T
-//    registers (the key order of the contraction is permuted to match the C
-//    layout) and V^T is read from the same staged rows with ds_read_b64_tr_b16
-//    (bf16) or ds_read_b64_tr_b8 (fp8) transposing loads.  O lives in 256
-//    accumulation registers per lane.
+//    HBM into LDS with 16-byte direct-to-LDS loads, through a ring of four
+//    slots: step j (QK), step j-1 (PV) and two steps in flight (three slots
+//    and one step in flight for bf16 top-k, whose resolved rows need the
+//    room).  The dense variants read page ids from the block table through
+//    the scalar cache.  The chunk order of each row is XOR-permuted by row so
+//    the operand reads below spread over the LDS banks.
+//  * Iteration j, behind one workgroup barrier: S^T[32 keys x 32 heads] =
+//    K Q^T for step j as one chain of 36 v_mfma_f32_32x32x16_bf16 (K read
+//    from LDS as the A operand), with the first PV MFMAs of step j-1 and the
+//    loads of step j+2 spread through it; then the softmax of step j
+//    interleaved with the remaining PV MFMAs of step j-1; then P of step j is
+//    written to LDS for every wave's PV.  Steady-state iterations are
+//    compiled without the checks for a unit's first and last steps.
+//  * Softmax in base 2 against a reference fixed at the unit's first-step
+//    max, so O is never rescaled in the loop; a logit more than 64 above the
+//    reference makes the workgroup redo the unit from its true max (at most
+//    two passes).  Numerator and denominator share the reference, so the
+//    result is the same function.
+//  * O^T[512 x heads] += V^T P^T on MFMA: P^T fragments come from the P
+//    exchange area in LDS and V^T is read from the same staged rows with
+//    ds_read_b64_tr_b16 (bf16) or ds_read_b64_tr_b8 (fp8) transposing loads.
 //  * fp8 cache: E4M3 codes convert exactly to bf16; the per-token scale is
 //    applied in fp32 to the score and to P before P is rounded for PV.
 //  * fp8 latent-row cache (656-byte rows: E4M3 latent with a power-of-two
@@ -48,6 +56,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
@@ -572,13 +581,18 @@ struct StepLayout {
   static constexpr int kData = LAT ? kRopeOff + kStepKeys * 128 : kStepKeys * kRowBytes;  // 20480 / 18432 / 36864
   static constexpr int kScaleT = kData + 1024;                                            // LAT
   static constexpr int kBuf = LAT ? kData + 1536 : FP8 ? kData + 256 : kData;             // + fp32 scales
-  // Ring slots: the step being multiplied (QK), the previous one (PV), and
-  // kDist steps in flight.
-  static constexpr int kSlots = FP8 ? 4 : 3;
-  static constexpr int kDist = kSlots - 2;
   // per wave and step (LAT: wave 0; waves 1-3 issue one fewer)
   static constexpr int kLoadsPerStep = LAT ? 6 : FP8 ? 5 : 9;
-  static constexpr int kRing = kSlots * kBuf;
+};
+
+// Ring slots of the attend kernel: the step being multiplied (QK), the
+// previous one (PV), and kDist steps in flight.  Four slots (two steps in
+// flight) everywhere except the bf16 top-k variant, whose resolved pool rows
+// take the LDS the fourth slot would need.
+template <bool FP8, bool TOPK>
+struct Ring {
+  static constexpr int kSlots = (FP8 || !TOPK) ? 4 : 3;
+  static constexpr int kDist = kSlots - 2;
 };
 
 // LDS map beyond the ring (bytes)
@@ -911,14 +925,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   static_assert(!LAT || FP8, "latent rows are an fp8 variant");
   using L = StepLayout<FP8, LAT>;
-  constexpr int kPOff = L::kRing;                    // P exchange area, two steps
-  constexpr int kLOff = kPOff + 2 * kPBytes;         // per-head normaliser, 128 floats
-  constexpr int kBtOff = kLOff + kMaxHeads * 4;      // block-table slice (top-k: the unit's pool rows)
-  constexpr int kSmem = kBtOff + (TOPK ? kTopkUnitPages * kPage : kMaxUnitPages) * 4;
-  static_assert(kSmem <= 163840 - 64, "LDS budget");
+  constexpr int kSlots = Ring<FP8, TOPK>::kSlots, kDist = Ring<FP8, TOPK>::kDist;
+  constexpr int kRing = kSlots * L::kBuf;
+  // LDS map: the ring, then the P exchange area (two steps), then (top-k
+  // only) the unit's resolved pool rows.  The dense variants read their page
+  // ids from the block table in memory through the scalar cache, which is
+  // what lets the bf16 ring hold four 36-KB steps in the 160 KB.  Inside the
+  // ring, where nothing else lives at those times: the next unit record in
+  // the last 64 bytes (written between units; the slot is next filled by the
+  // DMA of step kSlots - 1, issued after two barriers), and during the
+  // epilogue the staged rows followed by the per-head normaliser.
+  constexpr int kPOff = kRing;
+  constexpr int kBtOff = kPOff + 2 * kPBytes;
+  constexpr int kSmem = kBtOff + (TOPK ? kTopkUnitPages * kPage * 4 : 0);
+  static_assert(kSmem <= 163840, "LDS budget");
+  constexpr int kStageRow = 128 * 4 + 16;            // epilogue: bytes per head, padded off the banks
+  constexpr int kLOff = 4 * 32 * kStageRow;          // epilogue: per-head normaliser, 128 floats
+  constexpr int kUnitOff = kRing - 64;
+  static_assert(kLOff + kMaxHeads * 4 <= kUnitOff, "epilogue staging, normaliser and unit record fit in the ring");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
-  __shared__ int4 s_unit;
-  __shared__ int32_t s_restart;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -927,13 +952,13 @@ void attend_kernel(AttendLaunch a) {
   const int head = 32 * wave + n32;
   const bool head_ok = head < a.H;
   const int32_t num_units = a.ws.header[kHdrUnits];
-  if (tid == 0) s_restart = 0;
   const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
   uint8_t LDS_AS* p_lds = sm + kPOff;
   float LDS_AS* l_lds = (float LDS_AS*)(sm + kLOff);
-  int32_t LDS_AS* s_bt = (int32_t LDS_AS*)(sm + kBtOff);
+  int32_t LDS_AS* s_bt = (int32_t LDS_AS*)(sm + kBtOff);  // top-k only
+  i32x4 LDS_AS* s_unit = (i32x4 LDS_AS*)(sm + kUnitOff);
 
   // ---- per-lane offsets (bytes), fixed for the kernel ----
   uint32_t src_lane, dma_row, dma_slot;
@@ -996,10 +1021,11 @@ void attend_kernel(AttendLaunch a) {
   for (;; ++next) {
     if (tid == 0) {
       const int32_t u = own_run ? next : atomicAdd(&a.ws.header[kHdrGrab], 1);
-      s_unit = u < last ? a.ws.units[u] : make_int4(-1, 0, 0, 0);
+      const int4 r = u < last ? a.ws.units[u] : make_int4(-1, 0, 0, 0);
+      *s_unit = (i32x4){r.x, r.y, r.z, r.w};
     }
     __syncthreads();
-    const int4 unit = s_unit;
+    const i32x4 unit = *s_unit;
     if (unit.x < 0) break;
     const int tile = unit.x, slot = unit.w;
     // The explicit vmcnt waits below assume every older memory operation of
@@ -1032,10 +1058,11 @@ void attend_kernel(AttendLaunch a) {
         }
         s_bt[e] = row;
       }
-    } else {
-      const int32_t* bt = a.block_table + (size_t)b * a.bt_stride + p0;
-      for (int k = tid; k < p1 - p0; k += 256) s_bt[k] = bt[k];
     }
+    // dense variants: the unit's block-table entries, read through the
+    // scalar cache (the table is not written while the kernel runs)
+    typedef const int32_t __attribute__((address_space(4))) ConstI32;
+    ConstI32* bt_unit = (ConstI32*)(a.block_table + (size_t)b * a.bt_stride + p0);
 
     // Query fragments: B operands, k = dims 16ks + 8h + [0, 8), row = head
     bf16x8 qf[36];
@@ -1059,9 +1086,8 @@ void attend_kernel(AttendLaunch a) {
       const int key = key_begin + j * kStepKeys;
       return a.kv_scales + (size_t)phys * kPage + ((key >> 5) & 1) * kStepKeys;
     };
-    auto step_phys = [&](int j) {
-      return __builtin_amdgcn_readfirstlane(s_bt[((key_begin + j * kStepKeys) >> 6) - p0]);
-    };
+    // page of step j (two steps per page: key_begin is a page boundary)
+    auto step_phys = [&](int j) { return bt_unit[j >> 1]; };
     // top-k: pool row of the lane's staged row of step j, and (fp8) of the
     // token scale it loads; their addresses
     auto lane_row = [&](int j) { return s_bt[j * kStepKeys + dma_row]; };
@@ -1073,7 +1099,7 @@ void attend_kernel(AttendLaunch a) {
     // ring slot of step j; the offset is laundered so the compiler keeps one
     // scalar per step instead of deriving per-lane induction variables
     auto slot_buf = [&](int j) {
-      uint32_t off = (uint32_t)(j % L::kSlots) * L::kBuf;
+      uint32_t off = (uint32_t)(j % kSlots) * L::kBuf;
       asm volatile("" : "+s"(off));
       return sm + off;
     };
@@ -1090,7 +1116,7 @@ void attend_kernel(AttendLaunch a) {
       // Pipeline: step j is staged kDist steps ahead; iteration j runs QK of
       // step j together with PV of step j-1, then the softmax of step j.
 #pragma unroll
-      for (int j = 0; j < L::kDist; ++j)
+      for (int j = 0; j < kDist; ++j)
         if (j < nsteps) {
           if constexpr (TOPK) {
             issue_from_v<FP8, LAT>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave,
@@ -1110,44 +1136,47 @@ void attend_kernel(AttendLaunch a) {
       l_exact = 0.f;
       float tmax = -INFINITY;  // largest t = z*log2(e) - m_ref of this pass, per lane
 
-      // page of the step staged next: read from LDS one iteration early, made
-      // uniform only where the loads are issued
-      int next_phys = !TOPK && L::kDist < nsteps ? step_phys(L::kDist) : 0;
-      int next_phys_v = 0;
-      // top-k: the rows of the step staged next (per lane), read one
-      // iteration early like the page above
-      int next_row = TOPK && L::kDist < nsteps ? lane_row(L::kDist) : 0;
-      int next_srow = TOPK && L::kDist < nsteps ? scale_row(L::kDist) : 0;
-      int next_row_v = 0, next_srow_v = 0;
+      // page of the step staged next (dense): read one iteration early
+      int next_phys = !TOPK && kDist < nsteps ? step_phys(kDist) : 0;
+      // top-k: the rows of the step staged next (per lane), read from LDS one
+      // iteration early
+      int next_row = TOPK && kDist < nsteps ? lane_row(kDist) : 0;
+      int next_srow = TOPK && kDist < nsteps ? scale_row(kDist) : 0;
       // One pipeline iteration: staging wait, QK of step j (interleaved with
-      // half of PV of step j-1 and the loads of step j + kDist), then the
-      // softmax of step j interleaved with the other half of PV of step j-1.
-      auto qk_softmax = [&](int j, auto with_pv) {
+      // part of PV of step j-1 and the loads of step j + kDist), then the
+      // softmax of step j interleaved with the rest of PV of step j-1.
+      // pf_mode 1 (the steady state): step j + kDist exists, so it is staged
+      // here, and step j is not the last one (no history end inside it); 2:
+      // nothing left to stage; 0 (the first step): decided at run time.
+      auto qk_softmax = [&](int j, auto with_pv, auto pf_mode) {
         constexpr bool kPV = decltype(with_pv)::value;
+        constexpr int kPFM = decltype(pf_mode)::value;
         uint8_t LDS_AS* buf = slot_buf(j);                     // step j
-        uint8_t LDS_AS* vbuf = slot_buf(j + L::kSlots - 1);    // step j-1
+        uint8_t LDS_AS* vbuf = slot_buf(j + kSlots - 1);       // step j-1
         const uint8_t LDS_AS* p_prev = p_lds + kPBytes * ((j + 1) & 1);  // P of step j-1
         const int key0 = key_begin + j * kStepKeys;
-        const int valid = key_end - key0;  // >= 1
-        const bool pf_next = j + L::kDist < nsteps;
-        const int pf_phys = TOPK ? 0 : j == 0 ? next_phys : __builtin_amdgcn_readfirstlane(next_phys_v);
-        const uint8_t* pf_src = step_src(j + L::kDist, pf_phys);
-        const float* pf_scales = step_scales(j + L::kDist, pf_phys);
+        const int valid = key_end - key0;  // >= 1; >= 32 in the steady state
+        const bool pf_next = kPFM == 1 ? true : kPFM == 2 ? false : (j + kDist < nsteps);
+        const bool may_end = kPFM != 1;
+        const int pf_phys = TOPK ? 0 : next_phys;
+        const uint8_t* pf_src = step_src(j + kDist, pf_phys);
+        const float* pf_scales = step_scales(j + kDist, pf_phys);
         uint64_t pf_row = 0, pf_srow = 0;
-        const int32_t LDS_AS* pf_rows = s_bt + (j + L::kDist) * kStepKeys;  // top-k: rows of step j + kDist
+        const int32_t LDS_AS* pf_rows = s_bt + (j + kDist) * kStepKeys;  // top-k: rows of step j + kDist
         if constexpr (TOPK) {
-          pf_row = row_addr(j == 0 ? next_row : next_row_v);
-          pf_srow = scale_addr(j == 0 ? next_srow : next_srow_v);
+          pf_row = row_addr(next_row);
+          pf_srow = scale_addr(next_srow);
         }
-        uint8_t LDS_AS* pf_buf = slot_buf(j + L::kDist);
-        if (L::kDist == 2 && j + 1 < nsteps) {
-          // (LAT: only wave 0 loads the tile scales)
+        uint8_t LDS_AS* pf_buf = slot_buf(j + kDist);
+        if (kDist == 2 && (kPFM == 1 || j + 1 < nsteps)) {
+          // step j + 1's loads may still be in flight (LAT: only wave 0 loads
+          // the tile scales)
           if (LAT && wave != 0) wait_vmcnt<L::kLoadsPerStep - 1>();
           else wait_vmcnt<L::kLoadsPerStep>();
         } else {
           wait_vmcnt<0>();
         }
-        if (valid < kStepKeys) {
+        if (may_end && valid < kStepKeys) {
           // rows past the history end: P is zero there, V must not be NaN
           const u32x4 z = {0, 0, 0, 0};
           if ((int)opaque(dma_row) >= valid) {
@@ -1179,6 +1208,19 @@ void attend_kernel(AttendLaunch a) {
         // step j staged; P of step j-1 visible; every wave is done with
         // iteration j-1, so the slot of step j-2 is free
         lds_barrier();
+        // page (top-k: rows) of the step the next iteration stages, read now
+        // and used there; the index is clamped to the unit's last step.  (The
+        // scalar load is issued here, where the first K-fragment wait drains
+        // the LDS queue anyway: until it returns every LDS wait is a full one.)
+        if (kPFM != 2) {
+          const int jn = min(j + kDist + 1, nsteps - 1);
+          if constexpr (TOPK) {
+            next_row = lane_row(jn);
+            next_srow = scale_row(jn);
+          } else {
+            next_phys = step_phys(jn);
+          }
+        }
 
         // ---- stream 1: QK^T of step j for the wave's head block (36 MFMAs,
         // one K fragment each) with the first kPV1 MFMAs of PV of step j-1
@@ -1318,13 +1360,6 @@ void attend_kernel(AttendLaunch a) {
             sc[r >> 1] = *(const f32x2 LDS_AS*)(buf + L::kData + 4 * m);
           }
         }
-        // page of the step the next iteration stages (read now, used there)
-        if constexpr (TOPK) {
-          next_row_v = j + L::kDist + 1 < nsteps ? lane_row(j + L::kDist + 1) : 0;
-          next_srow_v = j + L::kDist + 1 < nsteps ? scale_row(j + L::kDist + 1) : 0;
-        } else {
-          next_phys_v = j + L::kDist + 1 < nsteps ? s_bt[((key_begin + (j + L::kDist + 1) * kStepKeys) >> 6) - p0] : 0;
-        }
 
         // ---- scores: token scales (fp8), the history-end mask and, on the
         // unit's first step, the reference.  Softmax in base 2; lane = one
@@ -1338,7 +1373,7 @@ void attend_kernel(AttendLaunch a) {
               sacc[r + 1] *= sc[r >> 1][1];
             }
           }
-          if (valid < kStepKeys) {
+          if (may_end && valid < kStepKeys) {
             // the last step of a history: keys past its end get no weight
             const int hk = (int)opaque(4 * h);
 #pragma unroll
@@ -1423,8 +1458,10 @@ void attend_kernel(AttendLaunch a) {
         }
       };
 
-      qk_softmax(0, std::false_type{});
-      for (int j = 1; j < nsteps; ++j) qk_softmax(j, std::true_type{});
+      qk_softmax(0, std::false_type{}, std::integral_constant<int, 0>{});
+      int j = 1;
+      for (; j + kDist < nsteps; ++j) qk_softmax(j, std::true_type{}, std::integral_constant<int, 1>{});
+      for (; j < nsteps; ++j) qk_softmax(j, std::true_type{}, std::integral_constant<int, 2>{});
       // PV of the last step
       lds_barrier();
       pv_stream<FP8, LAT>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o,
@@ -1432,14 +1469,17 @@ void attend_kernel(AttendLaunch a) {
       const float mt_max = fmaxf(tmax, wave_xor32(tmax));
       const float m_seen = m_ref + mt_max;
       const bool over = mt_max > 64.0f;
-      if (__builtin_amdgcn_ballot_w64(over) && lane == 0) s_restart = 1;
+      // Every wave votes in the P buffer the last step did not use: the last
+      // PV reads only the other one.  It is written next by the P of the
+      // first step of a second pass, behind that step's barrier, so every
+      // wave has read the votes by then.
+      int32_t LDS_AS* votes = (int32_t LDS_AS*)(p_lds + kPBytes * (nsteps & 1));
+      if (lane == 0) votes[wave] = __builtin_amdgcn_ballot_w64(over) ? 1 : 0;
       __syncthreads();
-      const bool restart = s_restart != 0;
-      __syncthreads();
+      const bool restart = (votes[0] | votes[1] | votes[2] | votes[3]) != 0;
       // the second pass starts from the unit's true max, so it never
       // overflows; it is the last one in any case
       if (!restart || pass > 0) break;
-      if (tid == 0) s_restart = 0;
       m_init = m_seen;
     }  // pass
 
@@ -1466,8 +1506,6 @@ void attend_kernel(AttendLaunch a) {
     // own 128 columns; its LDS ops complete in order, so no barrier is needed.
     // Accumulator lane: head 32hb + n32, columns 32cbl + 8q + 4h + [0, 4).
     {
-      constexpr int kStageRow = 128 * 4 + 16;  // bytes per head, padded off the banks
-      static_assert(4 * 32 * kStageRow <= L::kRing, "epilogue staging fits in the ring");
       // The addresses below are the same for every unit: laundering the lane
       // coordinates here keeps the compiler from hoisting all of them out of
       // the unit loop (and spilling them).
