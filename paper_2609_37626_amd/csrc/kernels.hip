@@ -598,6 +598,24 @@ struct Ring {
 // LDS map beyond the ring (bytes)
 constexpr int kPBytes = kMaxHeads * kStepKeys * 2;   // P for all heads, bf16
 
+// Placement of the 32 PV MFMAs of step j-1 in iteration j: kPV1 spread
+// through the QK chain of step j, kPVTail after P of step j is written, and
+// the last kPVDefer (column block 7) carried in registers past the next
+// barrier, where they cover the latency of that iteration's first K-fragment
+// reads; the softmax of step j rides on the rest.  Every accumulator keeps
+// its order, so the results do not depend on these counts.
+#ifndef SPLASH_PV1
+#define SPLASH_PV1 0
+#endif
+#ifndef SPLASH_PV_TAIL
+#define SPLASH_PV_TAIL 4
+#endif
+#ifndef SPLASH_PV_DEFER
+#define SPLASH_PV_DEFER 2
+#endif
+constexpr int kPV1 = SPLASH_PV1, kPVTail = SPLASH_PV_TAIL, kPVDefer = SPLASH_PV_DEFER;
+static_assert(kPV1 >= 0 && kPV1 <= 12 && kPVDefer >= 0 && kPVDefer <= 4 && kPVTail >= 0, "PV placement");
+
 // Direct global->LDS loads, issued through asm so that the compiler's wait
 // insertion (which cannot tell which LDS bytes they write) does not drain
 // them before every LDS read; the kernel waits for them explicitly.  The
@@ -880,7 +898,11 @@ __device__ __forceinline__ uint32_t p_slot(uint32_t hh, uint32_t kh, uint32_t ha
 template <bool FP8, bool LAT = false>
 __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint32_t (*vbase)[2],
                                           const uint8_t LDS_AS* p_lds, int wave, int n32, int h,
-                                          f32x16 (&o)[4][4], int lat_scales = 0) {
+                                          f32x16 (&o)[4][4], int lat_scales, const bf16x8& dv,
+                                          const bf16x8 (&dp)[4]) {
+  // the previous step's deferred MFMAs (column block 7)
+#pragma unroll
+  for (int hb = 4 - kPVDefer; hb < 4; ++hb) o[3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dv, dp[hb], o[3][hb], 0, 0, 0);
   // V fragments are double-buffered one column block ahead (c = 4kh + cbl).
   bf16x8 pf[4], vf[2];
   float psc[8];
@@ -927,22 +949,30 @@ void attend_kernel(AttendLaunch a) {
   using L = StepLayout<FP8, LAT>;
   constexpr int kSlots = Ring<FP8, TOPK>::kSlots, kDist = Ring<FP8, TOPK>::kDist;
   constexpr int kRing = kSlots * L::kBuf;
+  // Unit overlap (dense caches): the next unit's query and first kDist
+  // steps are issued before this unit's epilogue stores, so their latency
+  // hides behind the epilogue.
+  constexpr bool kOverlap = !TOPK && !LAT;
   // LDS map: the ring, then the P exchange area (two steps), then (top-k
   // only) the unit's resolved pool rows.  The dense variants read their page
   // ids from the block table in memory through the scalar cache, which is
-  // what lets the bf16 ring hold four 36-KB steps in the 160 KB.  Inside the
-  // ring, where nothing else lives at those times: the next unit record in
-  // the last 64 bytes (written between units; the slot is next filled by the
-  // DMA of step kSlots - 1, issued after two barriers), and during the
-  // epilogue the staged rows followed by the per-head normaliser.
+  // what lets the bf16 ring hold four 36-KB steps in the 160 KB.  The
+  // epilogue stages its rows, followed by the per-head normaliser, in LDS
+  // idle at that time: for bf16 in ring slots 0-1, with a unit's step j in
+  // slot (j + 2) mod 4 so that the next unit's first two steps land in slots
+  // 2-3 meanwhile; for fp8 after the P area; otherwise anywhere in the ring.
   constexpr int kPOff = kRing;
   constexpr int kBtOff = kPOff + 2 * kPBytes;
-  constexpr int kSmem = kBtOff + (TOPK ? kTopkUnitPages * kPage * 4 : 0);
-  static_assert(kSmem <= 163840, "LDS budget");
   constexpr int kStageRow = 128 * 4 + 16;            // epilogue: bytes per head, padded off the banks
   constexpr int kLOff = 4 * 32 * kStageRow;          // epilogue: per-head normaliser, 128 floats
-  constexpr int kUnitOff = kRing - 64;
-  static_assert(kLOff + kMaxHeads * 4 <= kUnitOff, "epilogue staging, normaliser and unit record fit in the ring");
+  constexpr int kStageBytes = kLOff + kMaxHeads * 4;
+  constexpr int kStageOff = (kOverlap && FP8) ? kBtOff : 0;
+  constexpr int kSlotBase = (kOverlap && !FP8) ? 2 : 0;
+  static_assert(!(kOverlap && !FP8) || kStageBytes <= 2 * L::kBuf, "bf16 staging fits in ring slots 0-1");
+  static_assert(kStageOff > 0 || kStageBytes <= kRing, "staging fits in the ring");
+  constexpr int kSmemA = kBtOff + (TOPK ? kTopkUnitPages * kPage * 4 : 0);
+  constexpr int kSmem = kSmemA > kStageOff + kStageBytes ? kSmemA : kStageOff + kStageBytes;
+  static_assert(kSmem <= 163840, "LDS budget");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -951,14 +981,12 @@ void attend_kernel(AttendLaunch a) {
   // QK and softmax role: head block `wave` (32 heads) over all 576 dims
   const int head = 32 * wave + n32;
   const bool head_ok = head < a.H;
-  const int32_t num_units = a.ws.header[kHdrUnits];
   const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
   uint8_t LDS_AS* p_lds = sm + kPOff;
-  float LDS_AS* l_lds = (float LDS_AS*)(sm + kLOff);
+  float LDS_AS* l_lds = (float LDS_AS*)(sm + kStageOff + kLOff);
   int32_t LDS_AS* s_bt = (int32_t LDS_AS*)(sm + kBtOff);  // top-k only
-  i32x4 LDS_AS* s_unit = (i32x4 LDS_AS*)(sm + kUnitOff);
 
   // ---- per-lane offsets (bytes), fixed for the kernel ----
   uint32_t src_lane, dma_row, dma_slot;
@@ -1012,38 +1040,78 @@ void attend_kernel(AttendLaunch a) {
     }
   }
 
-  // A fold plan made for this many workers gives each its own run of units;
-  // otherwise (or if the plan was made for another worker count) the workers
-  // draw units from the queue.
-  const bool own_run = a.ws.header[kHdrSchedule] == (int32_t)gridDim.x;
-  int32_t next = own_run ? a.ws.header[kHdrWorkerTable + blockIdx.x] : 0;
-  const int32_t last = own_run ? a.ws.header[kHdrWorkerTable + blockIdx.x + 1] : num_units;
-  for (;; ++next) {
-    if (tid == 0) {
-      const int32_t u = own_run ? next : atomicAdd(&a.ws.header[kHdrGrab], 1);
-      const int4 r = u < last ? a.ws.units[u] : make_int4(-1, 0, 0, 0);
-      *s_unit = (i32x4){r.x, r.y, r.z, r.w};
+  // Schedule, without atomics so that a worker knows its next unit ahead:
+  // under a fold plan made for this many workers, worker g runs its own
+  // units [table[g], table[g + 1]); otherwise the queue, ordered longest unit
+  // first, is dealt in a snake (pass k gives worker g position kG + g, or
+  // kG + G-1-g on odd passes), which pairs the longest units of one pass with
+  // the shortest of the next as a longest-first greedy schedule would.  The
+  // plan, the records and the lengths are read through the scalar cache:
+  // nothing writes them while the kernel runs.
+  typedef const int32_t __attribute__((address_space(4))) ConstI32;
+  typedef const i32x4 __attribute__((address_space(4))) ConstI32x4;
+  ConstI32* hdr = (ConstI32*)a.ws.header;
+  const int32_t G = (int32_t)gridDim.x, g = (int32_t)blockIdx.x;
+  const bool own_run = hdr[kHdrSchedule] == G;
+  const int32_t run_begin = own_run ? hdr[kHdrWorkerTable + g] : 0;
+  const int32_t run_end = own_run ? hdr[kHdrWorkerTable + g + 1] : hdr[kHdrUnits];
+  auto unit_rec = [&](int k) -> i32x4 {
+    const int32_t u = own_run ? run_begin + k : k * G + ((k & 1) ? G - 1 - g : g);
+    if (u < run_end) return ((ConstI32x4*)a.ws.units)[u];
+    return (i32x4){-1, 0, 0, 0};
+  };
+  // A unit's keys: request b, pages [p0, p1) (a shard's count from its first
+  // page), keys [key_begin, key_end) in nsteps steps of 32.
+  struct Geo {
+    int tile, slot, b, p0, p1, key_begin, key_end, nsteps;
+  };
+  auto geometry = [&](const i32x4 r) {
+    Geo u;
+    u.tile = r.x;
+    u.slot = r.w;
+    u.b = r.x / a.q_chunk;
+    const int qi = r.x - u.b * a.q_chunk;
+    int Lk = tile_keys(((ConstI32*)a.seq_lens)[u.b], a.q_chunk, qi);
+    u.p0 = r.y;
+    u.p1 = r.z;
+    if (a.key_end) {
+      const int first = ((ConstI32*)a.key_begin)[u.b] >> 6;
+      u.p0 += first;
+      u.p1 += first;
+      Lk = min(Lk, ((ConstI32*)a.key_end)[u.b]);
     }
-    __syncthreads();
-    const i32x4 unit = *s_unit;
-    if (unit.x < 0) break;
-    const int tile = unit.x, slot = unit.w;
-    // The explicit vmcnt waits below assume every older memory operation of
-    // this wave has completed (stores may complete out of order with loads).
-    wait_vmcnt<0>();
-    const int b = tile / a.q_chunk, qi = tile - b * a.q_chunk;
-    int Lk = tile_keys(a.seq_lens[b], a.q_chunk, qi);
-    int p0 = unit.y, p1 = unit.z;
-    if (a.key_end) {  // a shard: its pages count from the shard's first page
-      const int first = a.key_begin[b] >> 6;
-      p0 += first;
-      p1 += first;
-      Lk = min(Lk, a.key_end[b]);
+    if constexpr (TOPK) Lk = ((ConstI32*)a.topk_count)[r.x];  // entries of the row's list
+    u.key_begin = u.p0 * kPage;
+    u.key_end = min(u.p1 * kPage, Lk);
+    u.nsteps = (u.key_end - u.key_begin + kStepKeys - 1) / kStepKeys;
+    return u;
+  };
+  // Query fragments: B operands, k = dims 16ks + 8h + [0, 8), row = head.
+  // Padding heads (head >= H) take head 0's row: their scores stay finite and
+  // nothing of theirs is stored.  (Nothing consumes the loaded values here,
+  // so the loads stay in flight until the first QK MFMA.)
+  bf16x8 qf[36];
+  auto load_q = [&](int t) {
+    const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)t * a.H + (head_ok ? head : 0)) * kDimQK + 8 * h;
+#pragma unroll
+    for (int ks = 0; ks < 36; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + 16 * ks));
+  };
+
+  i32x4 cur = unit_rec(0), nxt = unit_rec(1);
+  bool pre = false;  // the current unit's query and first steps were issued by the previous unit
+  for (int k = 0; cur.x >= 0; ++k) {
+    const Geo U = geometry(cur);
+    const int tile = U.tile, slot = U.slot, b = U.b, p0 = U.p0, p1 = U.p1;
+    const int key_begin = U.key_begin, key_end = U.key_end, nsteps = U.nsteps;
+    // the record after next, and what the next unit needs at this unit's
+    // end, read now (scalar loads) and used there
+    const i32x4 nxt2 = unit_rec(k + 2);
+    Geo N = {};
+    int n_phys = 0;
+    if (kOverlap && nxt.x >= 0) {
+      N = geometry(nxt);
+      n_phys = ((ConstI32*)a.block_table)[(size_t)N.b * a.bt_stride + N.p0];
     }
-    if constexpr (TOPK) Lk = a.topk_count[tile];  // entries of the row's list
-    const int key_begin = p0 * kPage;
-    const int key_end = min(p1 * kPage, Lk);
-    const int nsteps = (key_end - key_begin + kStepKeys - 1) / kStepKeys;
 
     if constexpr (TOPK) {
       // pool row of every list entry of the unit (entries past the list end
@@ -1061,21 +1129,10 @@ void attend_kernel(AttendLaunch a) {
     }
     // dense variants: the unit's block-table entries, read through the
     // scalar cache (the table is not written while the kernel runs)
-    typedef const int32_t __attribute__((address_space(4))) ConstI32;
     ConstI32* bt_unit = (ConstI32*)(a.block_table + (size_t)b * a.bt_stride + p0);
 
-    // Query fragments: B operands, k = dims 16ks + 8h + [0, 8), row = head
-    bf16x8 qf[36];
-    {
-      const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)tile * a.H + (head_ok ? head : 0)) * kDimQK + 8 * h;
-#pragma unroll
-      for (int ks = 0; ks < 36; ++ks) {
-        u32x4 v = *(const u32x4*)(qrow + 16 * ks);
-        if (!head_ok) v = (u32x4){0, 0, 0, 0};  // padding heads
-        qf[ks] = __builtin_bit_cast(bf16x8, v);
-      }
-    }
-    __syncthreads();  // block-table slice visible
+    if (!pre) load_q(tile);
+    __syncthreads();  // (top-k) the resolved rows visible
 
     auto step_src = [&](int j, int phys) {
       const int key = key_begin + j * kStepKeys;
@@ -1099,7 +1156,7 @@ void attend_kernel(AttendLaunch a) {
     // ring slot of step j; the offset is laundered so the compiler keeps one
     // scalar per step instead of deriving per-lane induction variables
     auto slot_buf = [&](int j) {
-      uint32_t off = (uint32_t)(j % kSlots) * L::kBuf;
+      uint32_t off = (uint32_t)((j + kSlotBase) % kSlots) * L::kBuf;
       asm volatile("" : "+s"(off));
       return sm + off;
     };
@@ -1111,13 +1168,14 @@ void attend_kernel(AttendLaunch a) {
     // known after the first pass.
     float m_init = -INFINITY;
     f32x16 o[4][4];  // [column block cb - 4*wave][head block]
+    bf16x8 d_v, d_p[4];  // operands of the PV MFMAs carried past a barrier
     float m_ref, l_run, l_exact;
     for (int pass = 0;; ++pass) {
       // Pipeline: step j is staged kDist steps ahead; iteration j runs QK of
       // step j together with PV of step j-1, then the softmax of step j.
 #pragma unroll
       for (int j = 0; j < kDist; ++j)
-        if (j < nsteps) {
+        if (j < nsteps && (pass > 0 || !pre)) {
           if constexpr (TOPK) {
             issue_from_v<FP8, LAT>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave,
                                    s_bt + j * kStepKeys, kv);
@@ -1132,6 +1190,9 @@ void attend_kernel(AttendLaunch a) {
 #pragma unroll
         for (int y = 0; y < 4; ++y) o[x][y] = (f32x16){};
       m_ref = m_init;
+      d_v = (bf16x8){};
+#pragma unroll
+      for (int hb = 0; hb < 4; ++hb) d_p[hb] = (bf16x8){};
       l_run = 0.f;
       l_exact = 0.f;
       float tmax = -INFINITY;  // largest t = z*log2(e) - m_ref of this pass, per lane
@@ -1208,26 +1269,12 @@ void attend_kernel(AttendLaunch a) {
         // step j staged; P of step j-1 visible; every wave is done with
         // iteration j-1, so the slot of step j-2 is free
         lds_barrier();
-        // page (top-k: rows) of the step the next iteration stages, read now
-        // and used there; the index is clamped to the unit's last step.  (The
-        // scalar load is issued here, where the first K-fragment wait drains
-        // the LDS queue anyway: until it returns every LDS wait is a full one.)
-        if (kPFM != 2) {
-          const int jn = min(j + kDist + 1, nsteps - 1);
-          if constexpr (TOPK) {
-            next_row = lane_row(jn);
-            next_srow = scale_row(jn);
-          } else {
-            next_phys = step_phys(jn);
-          }
-        }
 
         // ---- stream 1: QK^T of step j for the wave's head block (36 MFMAs,
         // one K fragment each) with the first kPV1 MFMAs of PV of step j-1
         // spread among them (PV MFMA q: column block c = q >> 2 of key half
         // c >> 2, head block q & 3) and the loads of step j + kDist; the other
         // 32 - kPV1 PV MFMAs run under the softmax (stream 2).
-        constexpr int kPV1 = 8;
         f32x16 sacc;
         bf16x8 pf[4], pf1[4];
         float psc[2][8];  // LAT: tile-`wave` scales of the keys of pf / pf1
@@ -1243,6 +1290,13 @@ void attend_kernel(AttendLaunch a) {
 #pragma unroll
           for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_raw<FP8>(buf, kbase, ks);
           if constexpr (kPV) {
+            // the MFMAs step j-2 deferred, operands in registers, while the
+            // first K fragments arrive
+#pragma unroll
+            for (int hb = 4 - kPVDefer; hb < 4; ++hb) {
+              o[3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(d_v, d_p[hb], o[3][hb], 0, 0, 0);
+              __builtin_amdgcn_sched_barrier(0);
+            }
             if constexpr (LAT) load_p_scales(vbuf + L::kScaleT, 0, h, wave, psc[0]);
 #pragma unroll
             for (int hb = 0; hb < 4; ++hb) pf[hb] = *(const bf16x8 LDS_AS*)(p_prev + p_slot(32 * hb + n32, 0, h));
@@ -1332,11 +1386,20 @@ void attend_kernel(AttendLaunch a) {
               vf[cn % 3] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
             if constexpr (LAT) {
+              // each P fragment is scaled at its first use (column block 0
+              // or 4), here or, for the MFMAs placed there, in stream 1
+              if (c == 0) pf[hb] = scale_p(pf[hb], psc[0]);
               if (c == 4) pf1[hb] = scale_p(pf1[hb], psc[1]);
             }
             const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
             if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
-            o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
+            if (q >= 32 - kPVDefer) {
+              // carried past the next barrier
+              if (hb == 4 - kPVDefer) d_v = vcur;
+              d_p[hb] = pv;
+            } else {
+              o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
+            }
             // (as in stream 1) the key half 1 P fragment after the last read
             // of the half 0 one (LAT: with its key scales)
             if (c == 3) {
@@ -1350,7 +1413,7 @@ void attend_kernel(AttendLaunch a) {
         // kLead PV MFMAs run while the QK chain drains, the last kTail after
         // the P of step j is published (through the write and the next
         // barrier); the softmax rides on the rest
-        constexpr int kLead = kPV ? 2 : 0, kTail = kPV ? 2 : 0;
+        constexpr int kLead = kPV ? 2 : 0, kTail = kPV ? kPVTail + kPVDefer : 0;
         constexpr int kN2 = kPV ? 32 - kPV1 - kTail : 0;  // PV slots of stream 2
         f32x2 sc[8];
         if constexpr (FP8 && !LAT) {
@@ -1446,6 +1509,20 @@ void attend_kernel(AttendLaunch a) {
         }
         l_exact += pexact;
         l_run += (FP8 && !LAT) ? pexact : psum;
+        // page (top-k: rows) of the step the next iteration stages, read now
+        // and used there; the index is clamped to the unit's last step.  (The
+        // scalar load is issued after the last LDS wait of the iteration:
+        // until it returns every LDS wait is a full one, and the next one is
+        // the barrier's.)
+        if (kPFM != 2) {
+          const int jn = min(j + kDist + 1, nsteps - 1);
+          if constexpr (TOPK) {
+            next_row = lane_row(jn);
+            next_srow = scale_row(jn);
+          } else {
+            next_phys = step_phys(jn);
+          }
+        }
         // publish this wave's P^T (keys in slot order) for every wave's PV
         uint8_t LDS_AS* p_cur = p_lds + kPBytes * (j & 1);
         *(u32x4 LDS_AS*)(p_cur + p_slot(head, 0, h)) = (u32x4){pb[0], pb[1], pb[2], pb[3]};
@@ -1465,7 +1542,7 @@ void attend_kernel(AttendLaunch a) {
       // PV of the last step
       lds_barrier();
       pv_stream<FP8, LAT>(slot_buf(nsteps - 1), vbase, p_lds + kPBytes * ((nsteps - 1) & 1), wave, n32, h, o,
-                          L::kScaleT);
+                          L::kScaleT, d_v, d_p);
       const float mt_max = fmaxf(tmax, wave_xor32(tmax));
       const float m_seen = m_ref + mt_max;
       const bool over = mt_max > 64.0f;
@@ -1483,13 +1560,31 @@ void attend_kernel(AttendLaunch a) {
       m_init = m_seen;
     }  // pass
 
-    // ---- epilogue: normalise and store straight from the accumulators
+    // ---- the next unit's query and first steps.  Every wave is past its
+    // last PV (the vote barrier), so the ring is free; the epilogue below
+    // stages in LDS these steps do not use.  Steps 0 and 1 are the two halves
+    // of the unit's first page.
+    pre = false;
+    if constexpr (kOverlap) {
+      if (nxt.x >= 0) {
+        load_q(N.tile);
+#pragma unroll
+        for (int j = 0; j < kDist; ++j)
+          if (j < N.nsteps) issue_step<FP8, LAT>(step_src(j, n_phys), step_scales(j, n_phys), src_lane, slot_buf(j), wave);
+        pre = true;
+      }
+    }
+
+    // ---- epilogue: normalise and store
     {
       // normaliser: sum of the weights as applied (rounded); LSE: exact sum
       const float l_tot = l_run + wave_xor32(l_run);
       const float l_ex = l_exact + wave_xor32(l_exact);
       const float lse_nat = (m_ref + __log2f(l_ex)) * 0.6931471805599453f;
-      if (h == 0) l_lds[head] = l_tot;
+      // the reciprocal of each head's normaliser (1 ulp), by the wave that
+      // owns the head, at 32 hb + 16 (head & 1) + (head & 31) / 2: the
+      // store lanes below find their 16 rows of a head block contiguous
+      if (h == 0) l_lds[(head & ~31) + 16 * (head & 1) + ((head & 31) >> 1)] = __builtin_amdgcn_rcpf(l_tot);
       if (h == 0 && head_ok) {
         if (slot < 0) {
           if (a.lse) a.lse[(size_t)tile * a.H + head] = lse_nat;
@@ -1510,22 +1605,38 @@ void attend_kernel(AttendLaunch a) {
       // coordinates here keeps the compiler from hoisting all of them out of
       // the unit loop (and spilling them).
       const int hl = (int)opaque((uint32_t)h), nl = (int)opaque((uint32_t)n32);
-      const uint8_t LDS_AS* wstage = sm + wave * 32 * kStageRow;
+      const uint8_t LDS_AS* wstage = sm + kStageOff + wave * 32 * kStageRow;
       auto rows = [&](int hb, auto store) {
-        // rows 2k + h, 4 columns per lane: 32 lanes cover one head's 128;
-        // the row's normaliser (1 ulp reciprocal) is applied here
+        // rows 2k + h, 4 columns per lane: 32 lanes cover one head's 128,
+        // scaled by the row's reciprocal normaliser.  Rows go in batches of
+        // eight: their reads are issued together (the empty asm keeps them
+        // ahead of the stores), then their stores.  Heads past H are not
+        // stored: as H is a multiple of 16, the rows of head block hb to
+        // store are k < (H - 32 hb) / 2, a multiple of 8, the same for the
+        // whole wave.
+        f32x4 rl[4];
 #pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const int row = 2 * k + hl, hh = 32 * hb + row;
-          f32x4 v = *(const f32x4 LDS_AS*)(wstage + row * kStageRow + nl * 16);
-          v *= __builtin_amdgcn_rcpf(l_lds[hh]);
-          if (hh < a.H) store(hh, v);
+        for (int i = 0; i < 4; ++i) rl[i] = *(const f32x4 LDS_AS*)(l_lds + 32 * hb + 16 * hl + 4 * i);
+        const int kval = min(16, (a.H - 32 * hb) / 2);
+#pragma unroll 1
+        for (int k0 = 0; k0 < kval; k0 += 8) {
+          f32x4 v[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) v[k] = *(const f32x4 LDS_AS*)(wstage + (2 * (k0 + k) + hl) * kStageRow + nl * 16);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const f32x4 r = k0 ? rl[2 + (k >> 2)] : rl[k >> 2];
+            v[k] *= r[k & 3];
+            asm volatile("" : "+v"(v[k]));
+          }
+#pragma unroll
+          for (int k = 0; k < 8; ++k) store(32 * hb + 2 * (k0 + k) + hl, v[k]);
         }
       };
       const size_t col = 128 * wave + 4 * nl;
 #pragma unroll
       for (int hb = 0; hb < 4; ++hb) {
-        uint8_t LDS_AS* stage = sm + wave * 32 * kStageRow + nl * kStageRow + 16 * hl;
+        uint8_t LDS_AS* stage = sm + kStageOff + wave * 32 * kStageRow + nl * kStageRow + 16 * hl;
 #pragma unroll
         for (int cbl = 0; cbl < 4; ++cbl)
 #pragma unroll
@@ -1546,16 +1657,8 @@ void attend_kernel(AttendLaunch a) {
         }
       }
     }
-  }
-
-  // The last worker to drain the queue re-arms it, so one plan serves many runs.
-  if (tid == 0) {
-    __threadfence();
-    const int32_t done = atomicAdd(&a.ws.header[kHdrDone], 1);
-    if (done == (int32_t)gridDim.x - 1) {
-      atomicExch(&a.ws.header[kHdrGrab], 0);
-      atomicExch(&a.ws.header[kHdrDone], 0);
-    }
+    cur = nxt;
+    nxt = nxt2;
   }
 }
 
