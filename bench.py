@@ -61,32 +61,60 @@ def measured_traffic(workload):
     return None
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(batch, budget_s):
     """Time the fp64 oracle (as it stands) on the first requests of the batch,
-    then scale by visible (row, key) pairs to the whole batch."""
+    then scale by visible (row, key) pairs to the whole batch: once with the
+    BLAS threads numpy has on this host, once limited to one thread."""
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
     q = batch.q_chunk
     vis = [int(s) * q - q * (q - 1) // 2 for s in batch.seq_lens]
     total_vis = sum(vis)
-    done_vis, n, t_used = 0, 0, 0.0
-    while n < batch.B and t_used < budget_s:
-        t0 = time.perf_counter()
-        oracle.mla_attention(batch.q, batch.kv, batch.block_table, batch.seq_lens, q, batch.softmax_scale,
-                             kv_dtype=batch.kv_dtype, kv_scales=batch.kv_scales, requests=[n])
-        t_used += time.perf_counter() - t0
-        done_vis += vis[n]
-        n += 1
-    us_per_step = t_used * 1e6 * total_vis / done_vis
-    return {"value": round(us_per_step, 1), "unit": "us/step", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} of {batch.B} requests ({done_vis} of {total_vis} visible row-key pairs, "
-                      f"{t_used:.1f} s), scaled by visible row-key pairs",
-            "cpu_threads_available": len(os.sched_getaffinity(0))}
+
+    def timed(budget):
+        done_vis, n, t_used = 0, 0, 0.0
+        while n < batch.B and t_used < budget:
+            t0 = time.perf_counter()
+            oracle.mla_attention(batch.q, batch.kv, batch.block_table, batch.seq_lens, q, batch.softmax_scale,
+                                 kv_dtype=batch.kv_dtype, kv_scales=batch.kv_scales, requests=[n])
+            t_used += time.perf_counter() - t0
+            done_vis += vis[n]
+            n += 1
+        return t_used * 1e6 * total_vis / done_vis, n, done_vis, t_used
+
+    threads = os.cpu_count() or 1
+    one = None
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
+        with threadpool_limits(limits=1, user_api="blas"):
+            u1, n1, v1, t1 = timed(budget_s / 3)
+        one = {"value": round(u1, 1), "unit": "us/step", "cores": 1,
+               "sample": f"first {n1} of {batch.B} requests ({v1} of {total_vis} visible row-key pairs, "
+                         f"{t1:.1f} s), scaled by visible row-key pairs"}
+    except ImportError:
+        pass
+    us_per_step, n, done_vis, t_used = timed(budget_s)
+    res = {"value": round(us_per_step, 1), "unit": "us/step", "cores": int(threads), "kind": "oracle",
+           "sample": f"first {n} of {batch.B} requests ({done_vis} of {total_vis} visible row-key pairs, "
+                     f"{t_used:.1f} s), scaled by visible row-key pairs",
+           "cpu_model": cpu_model(), "cpu_threads_available": len(os.sched_getaffinity(0)),
+           "blas_threads": int(threads)}
+    if one is not None:
+        res["one_thread"] = one
+    return res
 
 
 def run_topk(args, spec, batch):
@@ -361,8 +389,6 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--cold-steps", type=int, default=10,
-                    help="extra steps, each after a 1 GiB write that evicts L2 and MALL (reported separately)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--topk", type=int, default=0,
@@ -390,8 +416,10 @@ def main():
     import torch
 
     from paper_2609_37626_amd import binding as B
+    from paper_2609_37626_amd import calib as CAL
     from paper_2609_37626_amd import workloads as W
     from paper_2609_37626_amd.device import to_device
+    globals()["B"], globals()["CAL"] = B, CAL
 
     assert torch.cuda.is_available(), "bench needs a GPU"
     spec = W.CONFIGS[args.config]
@@ -448,76 +476,97 @@ def main():
         warmup_run += 10
         torch.cuda.synchronize()
 
-    # Timed region: K steps back to back with nothing else on the stream.
+    # Warm region: K steps back to back with nothing else on the stream (the
+    # KV of one step can still sit partly in the 256 MB MALL for the next).
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
         step_plain()
     torch.cuda.synchronize()
-    wall_s = time.perf_counter() - t_start
-    ms_per_step = wall_s * 1e3 / args.steps
+    warm_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
 
-    # Instrumented pass right after it: the same K steps with HIP events on
-    # the launch stream around each kernel (per-kernel durations; the events
-    # themselves add a few microseconds per step, so value is not taken here).
+    # Same K steps with HIP events on the launch stream around each phase.
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for k in range(args.steps):
         step(events[k])
     torch.cuda.synchronize()
+    warm_ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] + [e[0].elapsed_time(e[3])]
+                        for e in events]) * 1e3
 
-    plan_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
-    attend_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
-    combine_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
-    step_ms = np.array([e[0].elapsed_time(e[3]) for e in events])
+    # Cold region (the headline): before each step the whole cache hierarchy
+    # (L2 and the 256 MB MALL) is flushed by READING a 1 GiB buffer, outside
+    # the events, so no dirty line is written back during the timed step.
+    flush_buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    flush_buf.zero_()
+    sink = torch.empty(512 * 1024, dtype=torch.uint8, device="cuda")
+    cev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        CAL.stream_read(flush_buf, sink, 512, stream)
+        step(cev[k])
+    torch.cuda.synchronize()
+    cold_wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
+    cold_ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] + [e[0].elapsed_time(e[3])]
+                        for e in cev]) * 1e3
+    del flush_buf
 
-    # Cold pass: the cache hierarchy (L2 + 256 MB MALL) is flushed before each
-    # step by writing a 1 GiB buffer outside the events.
-    cold = None
-    if args.cold_steps > 0:
-        scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.cold_steps)]
-        for k in range(args.cold_steps):
-            scratch.fill_(k & 0xFF)
-            step(cev[k])
-        torch.cuda.synchronize()
-        del scratch
-        cold = {"steps": args.cold_steps,
-                "step_us_median": round(float(np.median([e[0].elapsed_time(e[3]) for e in cev])) * 1e3, 2),
-                "attend_us_median": round(float(np.median([e[1].elapsed_time(e[2]) for e in cev])) * 1e3, 2)}
+    # Achievable peaks of this chip, measured in the same run: a streaming
+    # read of 1 GiB and a loop of bf16 MFMAs on random N(0,1) operands.
+    peaks = measured_peaks(torch, stream)
 
     offs, _ = B.workspace_offsets(batch.B, batch.q_chunk, batch.H, 0)
     hdr = ws[offs[0]:offs[0] + 64].cpu().numpy().view(np.int32)
 
     kv_bytes, alg_bytes, flops = W.workload_bytes_flops(batch)
-    attend_avg_s = float(attend_ms.mean()) * 1e-3
-    us = ms_per_step * 1e3
     hbm_time = alg_bytes / (HBM_PEAK_GBPS * 1e9)
     mfma_time = flops / (BF16_PEAK_TFLOPS * 1e12)
-    if hbm_time >= mfma_time:
-        achieved = alg_bytes / attend_avg_s / 1e9
+    roof_us = max(hbm_time, mfma_time) * 1e6
+    hbm_bound = hbm_time >= mfma_time
+
+    def pct(a, q):
+        return round(float(np.percentile(a, q)), 2)
+
+    cold_step, cold_att = np.median(cold_ph[:, 3]), np.median(cold_ph[:, 1])
+    warm_att = float(warm_ph[:, 1].mean())
+    us = float(cold_step)
+    if hbm_bound:
+        achieved = alg_bytes / (cold_att * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None}
+        measured_peak = peaks["stream_read_gbps"]
     else:
-        achieved = flops / attend_avg_s / 1e12
+        achieved = flops / (cold_att * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "traffic": None}
+        measured_peak = peaks["mfma_random_tflops"]
     traffic = measured_traffic(spec.name)
     if traffic is not None:
         roof["traffic"] = traffic["total_bytes"]
         roof["traffic_detail"] = traffic
-    roof.update({"kernel": "attend_kernel", "kernel_avg_us": round(attend_avg_s * 1e6, 2),
-                 "alg_bytes_per_launch": int(alg_bytes), "alg_flops_per_launch": int(flops),
-                 "roofline_us": round(max(hbm_time, mfma_time) * 1e6, 1)})
+    roof.update({
+        "kernel": "attend_kernel",
+        "kernel_avg_us": round(float(cold_att), 2),
+        "kernel_timing": "median over the cold steps (events on the launch stream)",
+        "frac_warm": round(roof_us / warm_att, 4),
+        "kernel_avg_us_warm": round(warm_att, 2),
+        "frac_whole_step": round(roof_us / us, 4),
+        "frac_whole_step_warm": round(roof_us / float(np.mean(warm_ph[:, 3])), 4),
+        "frac_of_measured_peak": round(roof["achieved"] / measured_peak, 4),
+        "alg_bytes_per_launch": int(alg_bytes), "alg_flops_per_launch": int(flops),
+        "roofline_us": round(roof_us, 1)})
 
     result = {
         "metric": METRIC,
         "value": round(us, 2),
         "unit": "us/step",
+        "value_kind": "median step (plan + attend + combine) over the cold steps: L2 and MALL flushed by a "
+                      "1 GiB read before each, outside the events",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "warmup_run": warmup_run,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(us * 1e-3, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -526,23 +575,27 @@ def main():
         "config": {"workload": spec.name, "B": batch.B, "H": batch.H, "q_chunk": batch.q_chunk,
                    "lengths": list(spec.lengths), "kv_cache": W.KV_LABELS[batch.kv_dtype],
                    "seed": spec.seed, "sum_seq_len": int(batch.seq_lens.sum()), "page_size": 64},
-        "kv_gbps": round(kv_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-        "alg_gbps": round(alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-        "tflops": round(flops / (ms_per_step * 1e-3) / 1e12, 1),
-        "step_event_us": {"mean": round(float(step_ms.mean()) * 1e3, 2),
-                          "p10": round(float(np.percentile(step_ms, 10)) * 1e3, 2),
-                          "p50": round(float(np.percentile(step_ms, 50)) * 1e3, 2),
-                          "p90": round(float(np.percentile(step_ms, 90)) * 1e3, 2)},
-        "phases_us": {"plan": round(float(plan_ms.mean()) * 1e3, 2),
-                      "attend": round(float(attend_ms.mean()) * 1e3, 2),
-                      "combine": round(float(combine_ms.mean()) * 1e3, 2)},
+        "kv_gbps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
+        "alg_gbps": round(alg_bytes / (us * 1e-6) / 1e9, 1),
+        "tflops": round(flops / (us * 1e-6) / 1e12, 1),
+        "cold": {"step_us": {"p10": pct(cold_ph[:, 3], 10), "p50": pct(cold_ph[:, 3], 50),
+                             "p90": pct(cold_ph[:, 3], 90)},
+                 "phases_us_median": {"plan": round(float(np.median(cold_ph[:, 0])), 2),
+                                      "attend": round(float(cold_att), 2),
+                                      "combine": round(float(np.median(cold_ph[:, 2])), 2)},
+                 "wall_us_per_step_incl_flush": round(cold_wall_ms * 1e3, 2)},
+        "warm": {"wall_us_per_step": round(warm_ms * 1e3, 2),
+                 "step_event_us": {"mean": round(float(warm_ph[:, 3].mean()), 2), "p10": pct(warm_ph[:, 3], 10),
+                                   "p50": pct(warm_ph[:, 3], 50), "p90": pct(warm_ph[:, 3], 90)},
+                 "phases_us_mean": {"plan": round(float(warm_ph[:, 0].mean()), 2),
+                                    "attend": round(warm_att, 2),
+                                    "combine": round(float(warm_ph[:, 2].mean()), 2)}},
         "plan": {"kind": "fold" if int(hdr[9]) > 0 else "unit size",
                  "units": int(hdr[1]), "partials": int(hdr[2]), "pages_per_unit": int(hdr[3]),
                  "fold_cap_pages": int(hdr[10]), "split_tiles": int(hdr[6]), "workers": B.device_workers()},
+        "measured_peaks": peaks,
         "roofline": roof,
     }
-    if cold is not None:
-        result["cold_cache"] = cold
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -554,6 +607,40 @@ def main():
         log("timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(batch, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def measured_peaks(torch, stream):
+    """Streaming-read bandwidth (1 GiB, non-temporal 16-byte loads, best of
+    five) and bf16 MFMA rate on random N(0,1) operands (every CU, four
+    chains per wave, best of three), from the calibration library."""
+    import numpy as np
+    G = B.device_workers()
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    buf.zero_()
+    sink = torch.empty(4 * G * 1024, dtype=torch.uint8, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    best_read = 0.0
+    for _ in range(5):
+        ev[0].record(stream)
+        CAL.stream_read(buf, sink, 2 * G, stream)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        best_read = max(best_read, (1 << 30) / (ev[0].elapsed_time(ev[1]) * 1e-3) / 1e9)
+    del buf
+    ops_bytes = CAL.mfma_ops_bytes(G)
+    g = torch.Generator(device="cuda").manual_seed(0)
+    ops = torch.randn(ops_bytes // 2, generator=g, device="cuda").to(torch.bfloat16)
+    iters = 1000
+    best_mfma = 0.0
+    for _ in range(3):
+        ev[0].record(stream)
+        CAL.mfma_loop(ops, iters, sink, G, stream)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        best_mfma = max(best_mfma, CAL.mfma_flops(G, iters) / (ev[0].elapsed_time(ev[1]) * 1e-3) / 1e12)
+    return {"stream_read_gbps": round(best_read, 1), "mfma_random_tflops": round(best_mfma, 1),
+            "how": "streaming read of 1 GiB (2 x CUs workgroups, best of 5); bf16 32x32x16 MFMA loop on "
+                   "random N(0,1) operands on every CU (best of 3)"}
 
 
 if __name__ == "__main__":

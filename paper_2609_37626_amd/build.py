@@ -13,6 +13,9 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libsplash_attn.so")
 SOURCES = ["api.cpp", "kernels.hip", "dop.hip"]
+# measurement helpers for the benchmark, a library of their own
+CALIB_LIB = os.path.join(HERE, "libsplash_calib.so")
+CALIB_SOURCES = ["calib.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -31,9 +34,14 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source into libsplash_attn.so (always rebuilds)."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc()] + HIPCC_FLAGS + [os.path.join(CSRC, s) for s in SOURCES] + ["-o", tmp]
+    """Compile libsplash_attn.so and libsplash_calib.so (always rebuilds)."""
+    _compile(CALIB_SOURCES, CALIB_LIB, verbose)
+    return _compile(SOURCES, LIB, verbose)
+
+
+def _compile(sources, lib, verbose: bool) -> str:
+    tmp = lib + ".tmp"
+    cmd = [hipcc()] + HIPCC_FLAGS + [os.path.join(CSRC, s) for s in sources] + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -43,8 +51,8 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
     if verbose and msgs:
         print("\n".join(msgs))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

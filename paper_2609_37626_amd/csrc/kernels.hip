@@ -1307,8 +1307,9 @@ void attend_kernel(AttendLaunch a) {
           for (int i = 0; i < 36; ++i) {
             // PV MFMA q of this slot, if any: slot (36q) / kPV1
             constexpr int kNone = -1;
+            constexpr int kPV1d = kPV1 > 0 ? kPV1 : 1;  // (no division by zero when kPV1 is 0)
             const int qc = (i * kPV1 + 35) / 36;
-            const int q = (kPV && qc < kPV1 && (qc * 36) / kPV1 == i) ? qc : kNone;
+            const int q = (kPV && qc < kPV1 && (qc * 36) / kPV1d == i) ? qc : kNone;
             if (q != kNone && (q & 3) == 0 && (q >> 2) + 2 < 8) {
               // V fragment two column blocks ahead (c = 4kh + cbl); its ring
               // entry last served column block c - 1
@@ -1339,7 +1340,7 @@ void attend_kernel(AttendLaunch a) {
                 if (c == 0) pf[hb] = scale_p(pf[hb], psc[0]);
               }
               const bf16x8 pv = c < 4 ? pf[hb] : pf1[hb];
-              if (hb == 0) vcur = frag_bf16<FP8>(vf[c % 3]);
+              if (hb == 0) vcur = frag_bf16<FP8>(vf[(c + 3) % 3]);
               o[c & 3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vcur, pv, o[c & 3][hb], 0, 0, 0);
               // key half 1 P fragment of this head block, in the registers
               // of the half 0 one, which column block 3 has just read last
