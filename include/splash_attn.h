@@ -153,6 +153,31 @@ int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_
                       void* stream);
 
 /*
+ * splash_mla_attend_noalloc: splash_mla_attend for callers that cannot
+ * allocate device memory (code under graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same step on a workspace the
+ * library owns, so the caller passes inputs and outputs only.
+ *   The workspace is a device array of SPLASH_NOALLOC_SCRATCH_BYTES inside
+ *   the library, one per GPU the library runs on, held until the process
+ *   ends; its address is looked up once per device.  The call allocates
+ *   nothing and enqueues only kernels on `stream`.
+ *   Every call on one GPU shares that GPU's array: calls that overlap on one
+ *   GPU (other streams, other threads) race and give undefined results;
+ *   calls in one stream order are fine.  Nothing in the array needs to
+ *   start at zero: the plan writes everything the later kernels read.
+ *   Arguments as for splash_mla_attend.  Errors: as splash_mla_attend, plus
+ *   SPLASH_ERR_WORKSPACE_TOO_SMALL when the batch's minimum workspace (its
+ *   plan, plus the partials that histories longer than 1024 pages force)
+ *   exceeds the array; with less room than splash_mla_attend's default
+ *   workspace the planner splits less.  SPLASH_FLAG_DEBUG_CHECK is refused
+ *   (SPLASH_ERR_UNSUPPORTED): its check reads a result back to the host.
+ */
+#define SPLASH_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int splash_mla_attend_noalloc(const void* q, const void* kv_pages, const int32_t* block_table,
+                              const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
+                              const splash_mla_desc* desc, void* stream);
+
+/*
  * splash_mla_plan + splash_mla_run: the same step in two halves, so that a
  * plan made once per step (it depends only on seq_lens, q_chunk and desc) can
  * serve every layer.  splash_mla_run must see the workspace of a plan made

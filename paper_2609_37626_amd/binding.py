@@ -66,6 +66,7 @@ _SIGNATURES = {
     "splash_mla_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
     "splash_mla_workspace_offsets": (_SZ, [_I32, _I32, _I32, _I32, ctypes.POINTER(_SZ)]),
     "splash_mla_attend": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
+    "splash_mla_attend_noalloc": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP]),
     "splash_mla_plan": (ctypes.c_int, [_VP, _I32, _PD, _VP, _SZ, _VP]),
     "splash_mla_run": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
     "splash_mla_attend_units": (ctypes.c_int, [_VP, _VP, _VP, _VP, _I32, _VP, _VP, _PD, _VP, _SZ, _VP]),
@@ -172,6 +173,16 @@ def splash_mla_attend(q, kv_pages, block_table, seq_lens, q_chunk: int, out, lse
     _check(lib().splash_mla_attend(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
                                    _ptr(out), _ptr(lse), ctypes.byref(desc), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def splash_mla_attend_noalloc(q, kv_pages, block_table, seq_lens, q_chunk: int, out, lse, desc: MlaDesc,
+                              stream=None) -> None:
+    """splash_mla_attend on the library's own workspace (no allocation)."""
+    _check(lib().splash_mla_attend_noalloc(_ptr(q), _ptr(kv_pages), _ptr(block_table), _ptr(seq_lens), q_chunk,
+                                           _ptr(out), _ptr(lse), ctypes.byref(desc), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20  # SPLASH_NOALLOC_SCRATCH_BYTES
 
 
 def splash_mla_plan(seq_lens, q_chunk: int, desc: MlaDesc, workspace, stream=None) -> None:

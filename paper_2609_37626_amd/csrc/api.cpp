@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -292,6 +293,32 @@ int dop_check(int64_t rows, int32_t hl, int32_t num_ranks, const void* const* pt
   return SPLASH_OK;
 }
 
+// Workspace of splash_mla_attend_noalloc: a device array of the library's
+// own, one copy on every GPU the library runs on, held until the process
+// ends.  In host code its name is only a stand-in, never a device address:
+// the address comes from hipGetSymbolAddress, taken once per device with
+// that device current, and only that address is passed on.
+static __device__ __align__(256) uint8_t scratch[SPLASH_NOALLOC_SCRATCH_BYTES];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];
+
+int scratch_for_current_device(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(SPLASH_ERR_UNSUPPORTED, "device %d: the scratch table holds 64 devices", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(SPLASH_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SPLASH_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -390,6 +417,28 @@ int splash_mla_attend(const void* q, const void* kv_pages, const int32_t* block_
     if ((st = check_device_data(kv_pages, block_table, seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   if ((st = do_plan(seq_lens, q_chunk, desc, wv, s)) != SPLASH_OK) return st;
   return do_run(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, wv, s);
+}
+
+int splash_mla_attend_noalloc(const void* q, const void* kv_pages, const int32_t* block_table,
+                              const int32_t* seq_lens, int32_t q_chunk, void* out, float* lse,
+                              const splash_mla_desc* desc, void* stream) {
+  int st = validate_desc(desc, q_chunk);
+  if (st != SPLASH_OK) return st;
+  if (desc->flags & SPLASH_FLAG_DEBUG_CHECK)
+    return fail(SPLASH_ERR_UNSUPPORTED,
+                "splash_mla_attend_noalloc: DEBUG_CHECK reads its result back to the host; use splash_mla_attend");
+  if (desc->batch == 0) return SPLASH_OK;
+  const int64_t T = (int64_t)desc->batch * q_chunk;
+  const size_t need = layout_for(T, desc->num_heads, forced_partials(T, desc->max_pages_per_seq)).total;
+  if (need > SPLASH_NOALLOC_SCRATCH_BYTES)
+    return fail(SPLASH_ERR_WORKSPACE_TOO_SMALL,
+                "splash_mla_attend_noalloc: this batch (%lld query rows, %d heads, up to %d pages per history) "
+                "needs at least %zu bytes of workspace; the library's scratch holds %zu: use splash_mla_attend",
+                (long long)T, desc->num_heads, desc->max_pages_per_seq, need, (size_t)SPLASH_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = scratch_for_current_device(&ws)) != SPLASH_OK) return st;
+  return splash_mla_attend(q, kv_pages, block_table, seq_lens, q_chunk, out, lse, desc, ws,
+                           SPLASH_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* block_table,

@@ -18,8 +18,8 @@ HEADER = os.path.join(ROOT, "include", "splash_attn.h")
 pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="library not built")
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=None):
+    text = open(header or HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(splash_\w+)\s*\(", text)))
 
@@ -36,6 +36,16 @@ def test_library_loads_and_exports_every_declared_symbol():
     missing = [n for n in declared_functions() if not hasattr(raw, n)]
     assert not missing, missing
     assert B.version().startswith("libsplash_attn")
+
+
+def test_calib_library_exports_every_declared_symbol():
+    from paper_2609_37626_amd import calib
+    header = os.path.join(os.path.dirname(HEADER), "splash_calib.h")
+    raw = ctypes.CDLL(calib.LIB_PATH)
+    names = declared_functions(header)
+    assert "splash_calib_stream_read" in names and "splash_calib_mfma_loop" in names
+    missing = [n for n in names if not hasattr(raw, n)]
+    assert not missing, missing
 
 
 FAKE = 1 << 20  # 16-byte aligned non-null address that is never dereferenced
@@ -349,3 +359,20 @@ def test_host_plan_queue_order(cfg, split):
     else:
         assert np.all(key[:-1] < key[1:])
     check_plan(seq, spec.q_chunk, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)
+
+
+def test_noalloc_refusals_happen_on_the_host():
+    """splash_mla_attend_noalloc refuses a batch whose minimum workspace
+    exceeds its scratch, and DEBUG_CHECK, before any HIP call; an empty
+    batch is a no-op."""
+    L = B.lib()
+
+    def call(desc):
+        return L.splash_mla_attend_noalloc(FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, ctypes.byref(desc), None)
+
+    # 600 histories of up to 2000 pages force 1200 partials of 256 KB each
+    assert call(B.make_desc(600, 128, 2000, 1 << 20)) == B.SPLASH_ERR_WORKSPACE_TOO_SMALL
+    assert "scratch holds" in L.splash_last_error().decode()
+    assert call(B.make_desc(4, 16, 8, 24, flags=B.FLAG_DEBUG_CHECK)) == B.SPLASH_ERR_UNSUPPORTED
+    assert call(B.make_desc(0, 16, 8, 24)) == B.SPLASH_OK
+    assert B.NOALLOC_SCRATCH_BYTES == 128 << 20
