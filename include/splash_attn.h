@@ -112,12 +112,13 @@ typedef struct splash_mla_desc {
  * SPLASH_DEFAULT_MAX_PARTIALS.  The planner never exceeds the capacity that
  * the passed ws_bytes provides: with too little room it splits less.
  * Layout (byte offsets from splash_mla_workspace_offsets, 256-byte aligned):
- *   [0] header int32[1152]: [0] unit counter, [1] number of work units,
- *       [2] partial slots used, [3] pages per unit chosen (0 for a fold
- *       plan), [4] debug status, [5] drained workers, [6] number of split
- *       tiles, [7] total pages, [8] most parts of a split tile, [9] workers of
- *       a fold plan (0: queue), [10] the fold plan's cap; from [64] the fold
- *       plan's first unit of each worker (workers + 1 entries)
+ *   [0] header int32[1152]: [1] number of work units, [2] partial slots
+ *       used, [3] pages per unit chosen (0 for a fold plan), [4] debug
+ *       status, [6] number of split tiles, [7] total pages, [8] most parts of
+ *       a split tile, [9] workers of a fold plan (0: the queue, ordered
+ *       longest unit first and dealt to the workers in a snake), [10] the fold
+ *       plan's cap; from [64] the fold plan's first unit of each worker
+ *       (workers + 1 entries).  [0] and [5] are written as 0 and unused.
  *   [1] work units int32[max_units][4] = {tile, first page, end page, slot},
  *       tile = b*q_chunk + i, slot = partial index or -1 (unit writes out/lse)
  *   [2] split offsets int32[B*q_chunk + 1] (partial slots of tile t are
@@ -136,7 +137,7 @@ size_t splash_mla_workspace_offsets(int32_t batch, int32_t q_chunk, int32_t num_
 /*
  * splash_mla_attend: the whole step -- plan, attend, combine -- on `stream`.
  *   q            bf16 [B*q_chunk, H, 576], row n = b*q_chunk + i, each head's 576
- *                entries packed [no-position 512 | rotary 64] (App. D)
+ *                entries packed [no-position 512 | rotary 64] (App. E)
  *   kv_pages     pool, see SPLASH_KV_*
  *   block_table  int32 [B, max_pages_per_seq]; logical page k of request b is
  *                physical page block_table[b*max_pages_per_seq + k]
@@ -273,7 +274,7 @@ int splash_dop_unpack_out(const void* recv, const int32_t* row_order, int32_t nu
                           int32_t heads_local, void* out, void* stream);
 
 /*
- * splash_mla_attend_shard: the partial result of one position shard (App. D,
+ * splash_mla_attend_shard: the partial result of one position shard (App. E,
  * position-sharded CP: each rank holds a slice of a request's token history,
  * and the ranks' partial results are merged by their log-sum-exp).  For every
  * query row n = b*q_chunk + i and head h it attends over the keys of request
@@ -305,7 +306,7 @@ int splash_mla_attend_shard(const void* q, const void* kv_pages, const int32_t* 
 /*
  * splash_mla_combine: merge partial attention results over disjoint key sets
  * into the result over their union (the merge a position-sharded history
- * needs, App. D).  For request b, partial slots s in
+ * needs, App. E).  For request b, partial slots s in
  * [split_indptr[b], split_indptr[b+1]) each hold rows i < q_chunk:
  *   partials     fp32 [S_tot, q_chunk, H, 512], normalised outputs
  *   partial_lse  fp32 [S_tot, q_chunk, H]; -inf marks a part with no key
@@ -335,7 +336,7 @@ int splash_mla_debug_gather(const void* kv_pages, const int32_t* block_table,
  * and `max_partials` partial slots.  units_out: int32 [max_units][4];
  * indptr_out: int32 [B*q_chunk + 1]; stats_out: int32[7] = {units, partial
  * slots used, pages per unit (0 for a fold plan), total pages, workers of a
- * fold plan (0: the workers draw units from a queue), the pages a fold plan
+ * fold plan (0: the queue, dealt to the workers in a snake), the pages a fold plan
  * lets a long history keep (the rest goes to a second worker), the most
  * parts of any split tile}; worker_start_out (may be NULL): int32
  * [num_workers + 1], for a fold plan the first unit of each worker (worker g

@@ -196,7 +196,7 @@ def merge_partials(parts_out, parts_lse):
     With L = ln sum_s exp(lse_s), out = sum_s exp(lse_s - L) * out_s.  Parts
     with lse = -inf (no visible key) weigh zero; if every part is empty the
     merge is empty too (lse = -inf, out = 0).  This is the merge a
-    position-sharded history needs (App. D, position-sharded CP).
+    position-sharded history needs (App. E, position-sharded CP).
     """
     parts_out = np.asarray(parts_out, dtype=np.float64)
     parts_lse = np.asarray(parts_lse, dtype=np.float64)

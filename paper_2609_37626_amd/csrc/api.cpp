@@ -464,8 +464,9 @@ int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* b
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->flags & SPLASH_FLAG_DEBUG_CHECK) {
     int32_t* res = wv.header + kHdrDebug;
+    const void* latent_kv = desc->kv_dtype == SPLASH_KV_FP8_LATENT ? kv_pages : nullptr;
     hipError_t e = launch_topk_check(block_table, seq_lens, topk_idx, topk_count, (int32_t)N, q_chunk, topk,
-                                     desc->max_pages_per_seq, desc->num_pages, res, s);
+                                     desc->max_pages_per_seq, desc->num_pages, latent_kv, res, s);
     if (e != hipSuccess) return hip_fail(e, "check launch");
     int32_t host = 0;
     e = hipMemcpyAsync(&host, res, sizeof host, hipMemcpyDeviceToHost, s);
@@ -473,8 +474,9 @@ int splash_mla_attend_topk(const void* q, const void* kv_pages, const int32_t* b
     if (e != hipSuccess) return hip_fail(e, "check readback");
     if (host != INT32_MAX)
       return fail(SPLASH_ERR_INVALID_ARGUMENT,
-                  "row %d: count outside [0, topk], a position outside the row's visible prefix, or its block-table "
-                  "entry outside [0, num_pages)",
+                  "row %d: count outside [0, topk], a position outside the row's visible prefix, its block-table "
+                  "entry outside [0, num_pages), or (latent-row cache) a listed row's tile scale that is not a "
+                  "positive power of two",
                   host - 1);
   }
   Shard sh;

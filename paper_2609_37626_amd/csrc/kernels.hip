@@ -473,10 +473,11 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   // unit finds its tile by binary search over the first-unit offsets; with
   // more units than workers the queue is ordered longest unit first (a
   // counting sort over unit lengths; the order among units of equal length
-  // is whatever the LDS atomics give, and does not change any result), so the
-  // persistent workers pack the units the way a longest-processing-time-first
-  // schedule would; with at most one unit per worker every unit starts at
-  // once: tile order.
+  // is whatever the LDS atomics give, and does not change any result); the
+  // attend kernel deals it to its workers in a snake, which pairs the longest
+  // units of one pass with the shortest of the next the way a
+  // longest-processing-time-first schedule would; with at most one unit per
+  // worker every unit starts at once: tile order.
   if (fold) {
     __syncthreads();  // partial offsets of every tile
     const int32_t r = tid;
@@ -1941,11 +1942,14 @@ __global__ void init_check(int32_t* result) { *result = INT32_MAX; }
 
 // Top-k variant: every row's count in [0, topk], every used position in the
 // row's visible prefix [0, s_b - q_chunk + i], and its page's block-table
-// entry in [0, num_pages).  Writes the smallest failing row + 1 (or 0).
+// entry in [0, num_pages); with the fp8 latent-row pool (latent_kv non-null)
+// also each listed row's four tile scales a positive normal power of two.
+// Writes the smallest failing row + 1 (or 0).
 __global__ __launch_bounds__(256) void topk_check_kernel(const int32_t* bt, const int32_t* seq_lens,
                                                          const int32_t* idx, const int32_t* count, int32_t N,
                                                          int32_t q_chunk, int32_t topk, int32_t bt_stride,
-                                                         int32_t num_pages, int32_t* result) {
+                                                         int32_t num_pages, const uint8_t* latent_kv,
+                                                         int32_t* result) {
   for (int n = blockIdx.x; n < N; n += gridDim.x) {
     const int b = n / q_chunk, i = n - b * q_chunk;
     const int s = seq_lens[b], c = count[n];
@@ -1958,7 +1962,17 @@ __global__ __launch_bounds__(256) void topk_check_kernel(const int32_t* bt, cons
           bad = true;
         } else {
           const int pg = bt[(size_t)b * bt_stride + (pos >> 6)];
-          if (pg < 0 || pg >= num_pages) bad = true;
+          if (pg < 0 || pg >= num_pages) {
+            bad = true;
+          } else if (latent_kv) {
+            const size_t row = (size_t)pg * kPage + (pos & (kPage - 1));
+            const u32x4 sc = *(const u32x4*)(latent_kv + row * kLatentRowBytes + 512);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const uint32_t ex = (sc[t] >> 23) & 0xFF;
+              if ((sc[t] & 0x807FFFFFu) != 0 || ex == 0 || ex == 0xFF) bad = true;
+            }
+          }
         }
       }
     }
@@ -2014,11 +2028,11 @@ hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_l
 
 hipError_t launch_topk_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* idx, const int32_t* count,
                              int32_t N, int32_t q_chunk, int32_t topk, int32_t bt_stride, int32_t num_pages,
-                             int32_t* result, hipStream_t s) {
+                             const void* latent_kv, int32_t* result, hipStream_t s) {
   hipLaunchKernelGGL(init_check, dim3(1), dim3(1), 0, s, result);
   int blocks = N < 1024 ? N : 1024;
   hipLaunchKernelGGL(topk_check_kernel, dim3(blocks), dim3(256), 0, s, bt, seq_lens, idx, count, N, q_chunk, topk,
-                     bt_stride, num_pages, result);
+                     bt_stride, num_pages, (const uint8_t*)latent_kv, result);
   return hipGetLastError();
 }
 

@@ -21,17 +21,17 @@ struct Workspace {
 
 // Header slots.
 enum HeaderSlot : int {
-  kHdrGrab = 0,        // unit counter the persistent workers draw from
+  kHdrGrab = 0,        // unused (written as 0)
   kHdrUnits = 1,       // number of work units
   kHdrPartials = 2,    // partial slots used
   kHdrChunk = 3,       // pages per unit
   kHdrDebug = 4,       // device-data check result (0 ok, else first failing item + 1)
-  kHdrDone = 5,        // workers that have drained the queue
+  kHdrDone = 5,        // unused (written as 0)
   kHdrSplitTiles = 6,  // number of tiles with partials
   kHdrTotalPages = 7,
   kHdrMaxParts = 8,    // upper bound on the parts of any split tile
-  kHdrSchedule = 9,    // 0: workers draw units from the queue; G > 0: fold plan for G workers,
-                       // worker g runs units [table[g], table[g + 1])
+  kHdrSchedule = 9,    // 0: the queue (longest unit first), dealt to the G workers in a snake;
+                       // G > 0: fold plan for G workers, worker g runs units [table[g], table[g + 1])
   kHdrFoldCap = 10,    // fold plan: pages a long tile keeps (its tail goes to a partner worker)
   kHdrWorkerTable = 64,  // fold plan: first unit of each worker, G + 1 entries
 };
@@ -88,7 +88,7 @@ hipError_t launch_gather(const void* kv, const int32_t* bt, const int32_t* seq_l
                          int32_t bt_stride, int32_t row_bytes, void* dense, hipStream_t s);
 hipError_t launch_topk_check(const int32_t* bt, const int32_t* seq_lens, const int32_t* idx, const int32_t* count,
                              int32_t N, int32_t q_chunk, int32_t topk, int32_t bt_stride, int32_t num_pages,
-                             int32_t* result, hipStream_t s);
+                             const void* latent_kv, int32_t* result, hipStream_t s);
 hipError_t launch_dop_pack_q(const void* q_nope, const void* q_rope, const int32_t* order, int32_t n, int32_t hl,
                              void* send, hipStream_t s);
 hipError_t launch_dop_unpack_q(const void* recv, int32_t T, int32_t n, int32_t hl, void* q_owner, hipStream_t s);

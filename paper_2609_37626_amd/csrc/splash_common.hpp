@@ -34,8 +34,8 @@ constexpr int kPlanLdsTiles = 8192;  // planner: tile data cached in LDS, and th
 // ceil(L/64) pages.  The planner cuts each tile's page range into units of at
 // most c pages; a tile cut into more than one unit writes fp32 partials that
 // the combine step merges.  c is chosen by an argmin of an estimated step
-// time over candidate sizes.  The G persistent workers take units from a
-// queue, so with W units the busiest worker runs R = ceil(W / G) of them: the
+// time over candidate sizes.  The G persistent workers are dealt the units of
+// a queue, so with W units the busiest worker runs R = ceil(W / G) of them: the
 // estimate is max(R * c, work / G) plus, per unit on that worker, a fixed
 // cost (query load, pipeline fill), per split unit on it the partial write,
 // and the combine's read of all S partials spread over the workers; all in
@@ -120,7 +120,7 @@ SPLASH_HD int64_t plan_cost(int32_t c, int64_t W, int64_t S, int64_t total_pages
   const int64_t c_eff = c < max_pages ? c : max_pages;
   const int64_t mean = total_pages * 16;
   // Busiest worker: at most R units of at most c_eff pages, never below the
-  // mean.  (The queue hands out the longest units first; a finer estimate of
+  // mean.  (The queue deals the longest units first; a finer estimate of
   // that packing favoured splitting batches of short histories, but measured
   // the saving did not cover the partial writes and the combine.)
   int64_t busy = R * c_eff * 16 * G;

@@ -139,3 +139,32 @@ def test_latent_topk_against_oracle(k, q_chunk):
     idx, cnt = lists(batch, k, np.random.default_rng(k), empty_rows=(1,), recent=8)
     out, lse = run_topk(batch, idx, cnt)
     check(batch, idx, cnt, out, lse, f"latent top-k k={k} q={q_chunk}")
+
+
+def test_topk_debug_check_rejects_listed_scales_that_are_not_powers_of_two():
+    # DEBUG_CHECK of the top-k entry checks the tile scales of every listed
+    # row; a row nobody lists may hold anything
+    from tests.test_gpu_topk import run_topk
+    batch = W.make_custom([300, 200], H=16, kv_dtype=LAT, seed=74)
+    N = batch.B
+    idx = np.full((N, 4), -1, dtype=np.int32)
+    idx[0, :3] = [5, 130, 299]
+    idx[1, :2] = [0, 199]
+    cnt = np.array([3, 2], dtype=np.int32)
+    out_ref, lse_ref = run_topk(batch, idx, cnt)
+    out_dbg, lse_dbg = run_topk(batch, idx, cnt, flags=B.FLAG_DEBUG_CHECK)   # valid data passes, same result
+    assert torch.equal(out_ref.view(torch.int16), out_dbg.view(torch.int16)) and torch.equal(lse_ref, lse_dbg)
+
+    def row_of(b, pos):
+        return int(batch.block_table[b, pos // 64]), pos % 64
+
+    for (b, pos), value in [((0, 130), 3.0), ((1, 199), -0.5), ((0, 5), 0.0), ((1, 0), np.inf)]:
+        page, r = row_of(b, pos)
+        kv = batch.kv.copy()
+        kv[page, r, 512 + 8:512 + 12] = np.array([value], dtype='<f4').view(np.uint8)   # tile 2
+        with pytest.raises(B.SplashError):
+            run_topk(dataclasses.replace(batch, kv=kv), idx, cnt, flags=B.FLAG_DEBUG_CHECK)
+    page, r = row_of(0, 6)   # position 6 of history 0 is not listed
+    kv = batch.kv.copy()
+    kv[page, r, 512:528] = np.full(4, 3.0, dtype='<f4').view(np.uint8)
+    run_topk(dataclasses.replace(batch, kv=kv), idx, cnt, flags=B.FLAG_DEBUG_CHECK)

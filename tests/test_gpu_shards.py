@@ -1,7 +1,7 @@
 """GPU parity of position shards (splash_mla_attend_shard + splash_mla_combine).
 
 A shard holds the keys [key_begin[b], key_end[b]) of each request's history
-(App. D, position-sharded CP).  Each shard's partial result is checked against
+(App. E, position-sharded CP).  Each shard's partial result is checked against
 the oracle restricted to those keys, and the merge of all shards against the
 oracle over the whole history.  Tolerances are the parity bar's (outputs
 max-abs 1e-2 for bf16 caches, 3e-2 for fp8; LSE 1e-3); rows with no key in a
