@@ -184,11 +184,13 @@ def draw_lengths(rng: np.random.Generator, spec: ConfigSpec) -> np.ndarray:
 
 def build_batch(rng: np.random.Generator, seq_lens, H: int, q_chunk: int,
                 kv_dtype: int = KV_BF16, unused_slot: int = -1,
-                extra_pages: int = 0) -> Batch:
+                extra_pages: int = 0, latent_exp=(-3, 0)) -> Batch:
     """Draw pool and queries for given lengths, following the recipe above.
 
     ``extra_pages`` appends never-referenced pages to the pool (their rows are
-    drawn too); ``unused_slot`` fills block-table slots past each history.
+    drawn too); ``unused_slot`` fills block-table slots past each history;
+    ``latent_exp`` is the range (ends included) of the latent-row tile
+    exponents u of step 5.
     """
     seq_lens = np.asarray(seq_lens, dtype=np.int32)
     B = int(seq_lens.shape[0])
@@ -210,9 +212,10 @@ def build_batch(rng: np.random.Generator, seq_lens, H: int, q_chunk: int,
         kv, scales = encode_e4m3_per_token(pool)
     elif kv_dtype == KV_FP8_LATENT:
         # 5. (this format only) every 128-column latent tile of every row is
-        # multiplied by 2^u, u uniform in [-3, 0], so that tile scales differ
-        # within a row and across rows while values stay at the N(0,1) scale
-        u = rng.integers(-3, 0, size=(num_pages, PAGE, 4), endpoint=True)
+        # multiplied by 2^u, u uniform in [-3, 0] (latent_exp), so that tile
+        # scales differ within a row and across rows while values stay at the
+        # N(0,1) scale
+        u = rng.integers(latent_exp[0], latent_exp[1], size=(num_pages, PAGE, 4), endpoint=True)
         pool[..., :DIM_V] *= np.repeat(np.ldexp(np.float32(1.0), u).astype(np.float32), 128, axis=-1)
         kv = np.concatenate([encode_fp8_latent_rows(pool[i:i + 256]) for i in range(0, num_pages, 256)]) \
             if num_pages else np.zeros((0, PAGE, LATENT_ROW_BYTES), np.uint8)
@@ -248,10 +251,10 @@ KV_LABELS = {KV_BF16: "bf16", KV_FP8_E4M3: "fp8-e4m3+fp32 scale",
 
 
 def make_custom(seq_lens, H: int, q_chunk: int = 1, kv_dtype: int = KV_BF16,
-                seed: int = 0, unused_slot: int = -1, extra_pages: int = 0) -> Batch:
+                seed: int = 0, unused_slot: int = -1, extra_pages: int = 0, latent_exp=(-3, 0)) -> Batch:
     """Batch with explicit lengths (parity cases, edge cases)."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    return build_batch(rng, seq_lens, H, q_chunk, kv_dtype, unused_slot, extra_pages)
+    return build_batch(rng, seq_lens, H, q_chunk, kv_dtype, unused_slot, extra_pages, latent_exp)
 
 
 def poison_unused_rows(batch: Batch) -> Batch:

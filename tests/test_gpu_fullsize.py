@@ -71,3 +71,31 @@ def test_full_size_workload_sampled_rows(cfg):
     print(f"  {len(samples)} sampled rows: out max-abs {err_o:.3e}  lse max-abs {err_l:.3e}", flush=True)
     assert err_o <= OUT_TOL[batch.kv_dtype]
     assert err_l <= LSE_TOL
+
+
+def test_single_history_of_524288_tokens():
+    """One request of 524,288 keys (8,192 pages: twice the paper's 256K
+    evaluation context, App. C), decode, 128 heads: the history is cut into
+    many units and their partials combined.  Sampled heads against the
+    oracle evaluated from the definition."""
+    batch = W.make_custom([524288], H=128, seed=91)
+    db = to_device(batch)
+    out, lse = db.alloc_outputs()
+    ws = db.workspace()
+    B.splash_mla_attend(db.q, db.kv, db.block_table, db.seq_lens, 1, out, lse, db.desc(), ws)
+    torch.cuda.synchronize()
+    offs, _ = B.workspace_offsets(1, 1, 128, 0)
+    hdr = ws[offs[0]:offs[0] + 32].cpu().numpy().view(np.int32)
+    print(f"  plan: {int(hdr[1])} units, {int(hdr[2])} partials", flush=True)
+    assert int(hdr[2]) > 8   # more than a unit may hold: split
+    o = out.float().cpu().numpy()
+    l = lse.cpu().numpy()
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
+    samples = [(0, 0, h) for h in (0, 1, 31, 64, 100, 127)]
+    ref_o, ref_l = oracle.mla_attention_sampled(batch.q, batch.kv, batch.block_table, batch.seq_lens, 1,
+                                                batch.softmax_scale, samples)
+    got_o = np.stack([o[0, h] for _, _, h in samples])
+    got_l = np.array([l[0, h] for _, _, h in samples])
+    err_o, err_l = np.abs(got_o - ref_o).max(), np.abs(got_l - ref_l).max()
+    print(f"  524288 keys, {len(samples)} heads: out max-abs {err_o:.3e}  lse max-abs {err_l:.3e}", flush=True)
+    assert err_o <= OUT_TOL[W.KV_BF16] and err_l <= LSE_TOL

@@ -168,3 +168,22 @@ def test_topk_debug_check_rejects_listed_scales_that_are_not_powers_of_two():
     kv = batch.kv.copy()
     kv[page, r, 512:528] = np.full(4, 3.0, dtype='<f4').view(np.uint8)
     run_topk(dataclasses.replace(batch, kv=kv), idx, cnt, flags=B.FLAG_DEBUG_CHECK)
+
+
+def test_latent_tile_exponents_up_to_three():
+    """Tile exponents u in [-3, 3] (scales 2^-10 ... 2^-3): latent values up to
+    8 times the N(0,1) scale, outputs up to tens.  Checked against a bar
+    relative to the magnitude: |out - ref| <= 3e-2 + 2^-7 |ref| (the fp8
+    absolute bar, plus the bf16 rounding of the output and of the weights,
+    each 2^-9 relative), |lse - ref| <= 1e-3 + 1e-5 |ref|."""
+    batch = W.make_custom([300, 1700, 65], H=64, q_chunk=2, kv_dtype=LAT, seed=75, latent_exp=(-3, 3))
+    out, lse = gpu_attend(batch)
+    ref_o, ref_l = run_oracle(batch)
+    o = out.float().cpu().numpy()
+    l = lse.cpu().numpy()
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
+    excess_o = np.abs(o - ref_o) - (3e-2 + 2.0 ** -7 * np.abs(ref_o))
+    excess_l = np.abs(l - ref_l) - (1e-3 + 1e-5 * np.abs(ref_l))
+    print(f"wide exponents: |ref out| max {np.abs(ref_o).max():.2f}; out max-abs {np.abs(o - ref_o).max():.3e}; "
+          f"worst excess over the bar {excess_o.max():.3e}; lse max-abs {np.abs(l - ref_l).max():.3e}", flush=True)
+    assert excess_o.max() <= 0 and excess_l.max() <= 0

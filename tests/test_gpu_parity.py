@@ -215,11 +215,17 @@ def _plan_lengths(case):
         "one_long": [262144],
         "long_and_short": [200000, 64, 65, 3000, 1],
         "equal_lengths": [4096] * 40,
-    }[case]
+    }.get(case)
+    if case == "over_8192_tiles":
+        # 2,100 requests of 4-row chunks: 8,400 tiles, more than the planner
+        # caches in LDS (the uncached path, units in tile order)
+        lens = np.random.Generator(np.random.PCG64(41)).integers(4, 400, size=2100, endpoint=True)
+        return lens.astype(np.int32), 4, 16
     return np.asarray(lens, dtype=np.int32), 1, 128
 
 
-@pytest.mark.parametrize("case", ["cfg2", "cfg3", "cfg4", "cfg5", "one_long", "long_and_short", "equal_lengths"])
+@pytest.mark.parametrize("case", ["cfg2", "cfg3", "cfg4", "cfg5", "one_long", "long_and_short", "equal_lengths",
+                                  "over_8192_tiles"])
 def test_device_plan_matches_host_plan(case):
     seq, q_chunk, H = _plan_lengths(case)
     Bn = len(seq)
@@ -249,7 +255,7 @@ def test_device_plan_matches_host_plan(case):
         assert np.array_equal(hdr[64:64 + G + 1], ws)
         runs = lambda u: [sorted((u[a:b, 2] - u[a:b, 1]).tolist()) for a, b in zip(ws[:-1], ws[1:])]
         assert runs(dev_units) == runs(units)
-    elif stats["units"] > G:
+    elif stats["units"] > G and Bn * q_chunk <= 8192:
         # the same units (the device leaves the order of equal-length units
         # open), and both queues hand out the longest units first
         canon = lambda u: u[np.lexsort(u.T[::-1])]
@@ -257,6 +263,10 @@ def test_device_plan_matches_host_plan(case):
         for u in (dev_units, units):
             ln = u[:, 2] - u[:, 1]
             assert np.all(ln[:-1] >= ln[1:])
+    elif stats["units"] > G:
+        # more tiles than the planner caches in LDS: the units in tile order
+        assert np.array_equal(dev_units, units)
+        assert np.all(np.diff(units[:, 0]) >= 0)
     else:
         # at most one unit per worker: tile order
         assert np.array_equal(dev_units, units)
@@ -325,3 +335,24 @@ def test_debug_check_rejects_bad_device_data():
     out, lse = good.attend(flags=B.FLAG_DEBUG_CHECK)
     torch.cuda.synchronize()
     assert_parity(batch, out, lse, label="debug check passes good data")
+
+
+def test_more_than_8192_tiles():
+    """8,400 tiles (2,100 requests x 4 chunk rows): the planner's uncached
+    path and the snake-dealt unit queue, against the oracle on sampled rows of
+    every kind (first, middle, last request; every chunk row; three heads)."""
+    lens, q_chunk, H = _plan_lengths("over_8192_tiles")
+    batch = W.make_custom(lens, H=H, q_chunk=q_chunk, seed=42)
+    out, lse = gpu_attend(batch)
+    o = out.float().cpu().numpy()
+    l = lse.cpu().numpy()
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
+    reqs = sorted({0, 1, 777, 1049, 1500, 2098, 2099, int(np.argmax(lens)), int(np.argmin(lens))})
+    samples = [(b, i, h) for b in reqs for i in range(q_chunk) for h in (0, 7, 15)]
+    ref_o, ref_l = oracle.mla_attention_sampled(batch.q, batch.kv, batch.block_table, batch.seq_lens, q_chunk,
+                                                batch.softmax_scale, samples)
+    got_o = np.stack([o[b * q_chunk + i, h] for b, i, h in samples])
+    got_l = np.array([l[b * q_chunk + i, h] for b, i, h in samples])
+    err_o, err_l = np.abs(got_o - ref_o).max(), np.abs(got_l - ref_l).max()
+    print(f"8400 tiles, {len(samples)} sampled rows: out max-abs {err_o:.3e}  lse max-abs {err_l:.3e}", flush=True)
+    assert err_o <= OUT_TOL[W.KV_BF16] and err_l <= LSE_TOL
