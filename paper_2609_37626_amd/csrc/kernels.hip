@@ -623,44 +623,50 @@ static_assert(kPV1 >= 0 && kPV1 <= 12 && kPVDefer >= 0 && kPVDefer <= 4 && kPVTa
 // source is a uniform 64-bit base plus a per-lane 32-bit offset; the LDS
 // destination is M0 + 16 * lane (4 * lane for the dword form).  No
 // instruction offset is used: it would move the LDS destination as well.
-// M0 is restored afterwards.
+// M0 is restored afterwards.  NT: the non-temporal hint ("nt" on gfx950),
+// which streams the lines through the caches instead of keeping them; the
+// attend kernel sets it when no other tile reads the same pages (one query
+// row per request), so that the cache rows do not evict what is reused.
+#define SPLASH_DMA_ASM(INSN, ADDR, HINT, SREG)                                               \
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, " SREG "\n\ts_nop 0\n\t" INSN " %1, " ADDR HINT \
+               "\n\ts_mov_b32 m0, %0"
+template <bool NT>
 __device__ __forceinline__ void dma_b128(const void* sbase, uint32_t voff, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(voff), "s"(sbase), "s"(m0)
-      : "memory");
+  if constexpr (NT)
+    SPLASH_DMA_ASM("global_load_lds_dwordx4", "%2", " nt", "%3") : "=&s"(saved) : "v"(voff), "s"(sbase), "s"(m0) : "memory");
+  else
+    SPLASH_DMA_ASM("global_load_lds_dwordx4", "%2", "", "%3") : "=&s"(saved) : "v"(voff), "s"(sbase), "s"(m0) : "memory");
 }
 // The same loads from a per-lane 64-bit address (gathered rows anywhere in
 // the pool).
+template <bool NT>
 __device__ __forceinline__ void dma_b128_v(uint64_t vaddr, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(vaddr), "s"(m0)
-      : "memory");
+  if constexpr (NT)
+    SPLASH_DMA_ASM("global_load_lds_dwordx4", "off", " nt", "%2") : "=&s"(saved) : "v"(vaddr), "s"(m0) : "memory");
+  else
+    SPLASH_DMA_ASM("global_load_lds_dwordx4", "off", "", "%2") : "=&s"(saved) : "v"(vaddr), "s"(m0) : "memory");
 }
+template <bool NT>
 __device__ __forceinline__ void dma_b32_v(uint64_t vaddr, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(vaddr), "s"(m0)
-      : "memory");
+  if constexpr (NT)
+    SPLASH_DMA_ASM("global_load_lds_dword", "off", " nt", "%2") : "=&s"(saved) : "v"(vaddr), "s"(m0) : "memory");
+  else
+    SPLASH_DMA_ASM("global_load_lds_dword", "off", "", "%2") : "=&s"(saved) : "v"(vaddr), "s"(m0) : "memory");
 }
+template <bool NT>
 __device__ __forceinline__ void dma_b32(const void* sbase, uint32_t voff, const uint8_t LDS_AS* lds) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(voff), "s"(sbase), "s"(m0)
-      : "memory");
+  if constexpr (NT)
+    SPLASH_DMA_ASM("global_load_lds_dword", "%2", " nt", "%3") : "=&s"(saved) : "v"(voff), "s"(sbase), "s"(m0) : "memory");
+  else
+    SPLASH_DMA_ASM("global_load_lds_dword", "%2", "", "%3") : "=&s"(saved) : "v"(voff), "s"(sbase), "s"(m0) : "memory");
 }
 
 // Issue the direct-to-LDS loads of one step.
@@ -672,13 +678,13 @@ __device__ __forceinline__ void dma_b32(const void* sbase, uint32_t voff, const 
 //        the 32 rows' tile scales.
 // step_src / step_scales are uniform; src_lane is the lane's byte offset
 // inside the step for t = 0.
-template <bool FP8, int t, bool LAT = false>
+template <bool FP8, int t, bool LAT, bool NT>
 __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                           uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
   if constexpr (LAT) {
     using L = StepLayout<true, true>;
     if constexpr (t < 4) {
-      dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+      dma_b128<NT>(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
     } else {
       // lane id from an asm (volatile: recomputed here, not held in a
       // register across the loop), then the lane's source offset
@@ -686,22 +692,22 @@ __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, 
       asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
       if constexpr (t == 4) {
         const uint32_t r = 8 * wave + (ln >> 3);
-        dma_b128(step_src, r * L::kRowBytes + 528 + (((ln & 7) ^ ((r >> 1) & 7)) * 16), buf + L::kRopeOff + 1024 * wave);
+        dma_b128<NT>(step_src, r * L::kRowBytes + 528 + (((ln & 7) ^ ((r >> 1) & 7)) * 16), buf + L::kRopeOff + 1024 * wave);
       } else if (wave == 0) {
-        dma_b128(step_src, (ln & 31) * L::kRowBytes + 512, buf + L::kData);  // lanes 32-63 repeat 0-31
+        dma_b128<NT>(step_src, (ln & 31) * L::kRowBytes + 512, buf + L::kData);  // lanes 32-63 repeat 0-31
       }
     }
   } else if constexpr (!FP8) {
-    dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 1024 * wave);
+    dma_b128<NT>(step_src + 128 * t, src_lane, buf + 4096 * t + 1024 * wave);
   } else {
     if (t < 4 || wave + 4 * t < 18) {
-      dma_b128(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+      dma_b128<NT>(step_src + 128 * t, src_lane, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
     } else {
       // byte offset of the lane's token scale, 4 (lane & 31), recomputed here
       // (volatile: not hoisted) rather than held in a register across the loop
       uint32_t voff;
       asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_and_b32 %0, 31, %0\n\tv_lshlrev_b32 %0, 2, %0" : "=v"(voff));
-      dma_b32(step_scales, voff, buf + 18432);
+      dma_b32<NT>(step_scales, voff, buf + 18432);
     }
   }
 }
@@ -712,56 +718,56 @@ __device__ __forceinline__ void issue_one(const uint8_t* __restrict__ step_src, 
 // loads take other rows of the step than the latent ones; their pool rows
 // are read here from step_rows (the step's 32 resolved rows in LDS), their
 // bytes from the pool at kv.
-template <bool FP8, int t, bool LAT = false>
+template <bool FP8, int t, bool LAT, bool NT>
 __device__ __forceinline__ void issue_one_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave,
                                             const int32_t LDS_AS* step_rows, const uint8_t* kv) {
   if constexpr (LAT) {
     using L = StepLayout<true, true>;
     if constexpr (t < 4) {
-      dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+      dma_b128_v<NT>(row_addr + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
     } else {
       uint32_t ln;
       asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
       const uint64_t base = (uint64_t)(uintptr_t)kv;
       if constexpr (t == 4) {
         const uint32_t r = 8 * wave + (ln >> 3);
-        dma_b128_v(base + (uint64_t)(uint32_t)step_rows[r] * L::kRowBytes + 528 + (((ln & 7) ^ ((r >> 1) & 7)) * 16),
+        dma_b128_v<NT>(base + (uint64_t)(uint32_t)step_rows[r] * L::kRowBytes + 528 + (((ln & 7) ^ ((r >> 1) & 7)) * 16),
                    buf + L::kRopeOff + 1024 * wave);
       } else if (wave == 0) {
-        dma_b128_v(base + (uint64_t)(uint32_t)step_rows[ln & 31] * L::kRowBytes + 512, buf + L::kData);
+        dma_b128_v<NT>(base + (uint64_t)(uint32_t)step_rows[ln & 31] * L::kRowBytes + 512, buf + L::kData);
       }
     }
   } else if constexpr (!FP8) {
-    dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 1024 * wave);
+    dma_b128_v<NT>(row_addr + 128 * t, buf + 4096 * t + 1024 * wave);
   } else {
     if (t < 4 || wave + 4 * t < 18)
-      dma_b128_v(row_addr + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
+      dma_b128_v<NT>(row_addr + 128 * t, buf + 4096 * t + 2048 * (wave >> 1) + 1024 * (wave & 1));
     else
-      dma_b32_v(scale_addr, buf + 18432);
+      dma_b32_v<NT>(scale_addr, buf + 18432);
   }
 }
-template <bool FP8, bool LAT, int t = 0>
+template <bool FP8, bool LAT, bool NT, int t = 0>
 __device__ __forceinline__ void issue_from_v(uint64_t row_addr, uint64_t scale_addr, uint8_t LDS_AS* buf, int wave,
                                              const int32_t LDS_AS* step_rows, const uint8_t* kv) {
   if constexpr (t < StepLayout<FP8, LAT>::kLoadsPerStep) {
-    issue_one_v<FP8, t, LAT>(row_addr, scale_addr, buf, wave, step_rows, kv);
-    issue_from_v<FP8, LAT, t + 1>(row_addr, scale_addr, buf, wave, step_rows, kv);
+    issue_one_v<FP8, t, LAT, NT>(row_addr, scale_addr, buf, wave, step_rows, kv);
+    issue_from_v<FP8, LAT, NT, t + 1>(row_addr, scale_addr, buf, wave, step_rows, kv);
   }
 }
 
-template <bool FP8, bool LAT, int t = 0>
+template <bool FP8, bool LAT, bool NT, int t = 0>
 __device__ __forceinline__ void issue_from(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                            uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
   if constexpr (t < StepLayout<FP8, LAT>::kLoadsPerStep) {
-    issue_one<FP8, t, LAT>(step_src, step_scales, src_lane, buf, wave);
-    issue_from<FP8, LAT, t + 1>(step_src, step_scales, src_lane, buf, wave);
+    issue_one<FP8, t, LAT, NT>(step_src, step_scales, src_lane, buf, wave);
+    issue_from<FP8, LAT, NT, t + 1>(step_src, step_scales, src_lane, buf, wave);
   }
 }
 
-template <bool FP8, bool LAT>
+template <bool FP8, bool LAT, bool NT>
 __device__ __forceinline__ void issue_step(const uint8_t* __restrict__ step_src, const float* __restrict__ step_scales,
                                            uint32_t src_lane, uint8_t LDS_AS* buf, int wave) {
-  issue_from<FP8, LAT>(step_src, step_scales, src_lane, buf, wave);
+  issue_from<FP8, LAT, NT>(step_src, step_scales, src_lane, buf, wave);
 }
 
 // QK^T MFMAs are issued through inline asm with a VGPR accumulator: the
@@ -943,7 +949,7 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
 // LAT: the fp8 latent-row cache (FP8 set too): latent tiles converted with
 // their tile scale for QK, the RoPE read as bf16, and for PV each wave's P
 // scaled by its tile's key scales.
-template <bool FP8, bool TOPK, bool LAT = false>
+template <bool FP8, bool TOPK, bool LAT, bool NT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   static_assert(!LAT || FP8, "latent rows are an fp8 variant");
@@ -1178,11 +1184,11 @@ void attend_kernel(AttendLaunch a) {
       for (int j = 0; j < kDist; ++j)
         if (j < nsteps && (pass > 0 || !pre)) {
           if constexpr (TOPK) {
-            issue_from_v<FP8, LAT>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave,
+            issue_from_v<FP8, LAT, NT>(row_addr(lane_row(j)), scale_addr(scale_row(j)), slot_buf(j), wave,
                                    s_bt + j * kStepKeys, kv);
           } else {
             const int ph = step_phys(j);
-            issue_step<FP8, LAT>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
+            issue_step<FP8, LAT, NT>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
           }
         }
 
@@ -1351,27 +1357,27 @@ void attend_kernel(AttendLaunch a) {
             if ((i & 3) == 1 && (i >> 2) < L::kLoadsPerStep && pf_next) {
               if constexpr (TOPK) {
                 switch (i >> 2) {
-                  case 0: issue_one_v<FP8, 0, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 1: issue_one_v<FP8, 1, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 2: issue_one_v<FP8, 2, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 3: issue_one_v<FP8, 3, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 4: issue_one_v<FP8, 4, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 5: issue_one_v<FP8, 5, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 6: issue_one_v<FP8, 6, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  case 7: issue_one_v<FP8, 7, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
-                  default: issue_one_v<FP8, 8, LAT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 0: issue_one_v<FP8, 0, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 1: issue_one_v<FP8, 1, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 2: issue_one_v<FP8, 2, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 3: issue_one_v<FP8, 3, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 4: issue_one_v<FP8, 4, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 5: issue_one_v<FP8, 5, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 6: issue_one_v<FP8, 6, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  case 7: issue_one_v<FP8, 7, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
+                  default: issue_one_v<FP8, 8, LAT, NT>(pf_row, pf_srow, pf_buf, wave, pf_rows, kv); break;
                 }
               } else {
                 switch (i >> 2) {
-                  case 0: issue_one<FP8, 0, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 1: issue_one<FP8, 1, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 2: issue_one<FP8, 2, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 3: issue_one<FP8, 3, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 4: issue_one<FP8, 4, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 5: issue_one<FP8, 5, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 6: issue_one<FP8, 6, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  case 7: issue_one<FP8, 7, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
-                  default: issue_one<FP8, 8, LAT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 0: issue_one<FP8, 0, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 1: issue_one<FP8, 1, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 2: issue_one<FP8, 2, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 3: issue_one<FP8, 3, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 4: issue_one<FP8, 4, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 5: issue_one<FP8, 5, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 6: issue_one<FP8, 6, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  case 7: issue_one<FP8, 7, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
+                  default: issue_one<FP8, 8, LAT, NT>(pf_src, pf_scales, src_lane, pf_buf, wave); break;
                 }
               }
             }
@@ -1572,7 +1578,7 @@ void attend_kernel(AttendLaunch a) {
         load_q(N.tile);
 #pragma unroll
         for (int j = 0; j < kDist; ++j)
-          if (j < N.nsteps) issue_step<FP8, LAT>(step_src(j, n_phys), step_scales(j, n_phys), src_lane, slot_buf(j), wave);
+          if (j < N.nsteps) issue_step<FP8, LAT, NT>(step_src(j, n_phys), step_scales(j, n_phys), src_lane, slot_buf(j), wave);
         pre = true;
       }
     }
@@ -1987,25 +1993,26 @@ hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+// NT (non-temporal cache-row loads) when every request has one query row:
+// then no two tiles read the same pages.
+template <bool FP8, bool TOPK, bool LAT>
+static void launch_attend_nt(const AttendLaunch& a, int32_t workers, hipStream_t s) {
+  if (a.q_chunk == 1)
+    hipLaunchKernelGGL((attend_kernel<FP8, TOPK, LAT, true>), dim3(workers), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((attend_kernel<FP8, TOPK, LAT, false>), dim3(workers), dim3(256), 0, s, a);
+}
+
 hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) {
   if (a.kv_dtype == 2) {
-    if (a.topk_idx) {
-      hipLaunchKernelGGL((attend_kernel<true, true, true>), dim3(workers), dim3(256), 0, s, a);
-    } else {
-      hipLaunchKernelGGL((attend_kernel<true, false, true>), dim3(workers), dim3(256), 0, s, a);
-    }
+    if (a.topk_idx) launch_attend_nt<true, true, true>(a, workers, s);
+    else launch_attend_nt<true, false, true>(a, workers, s);
   } else if (a.kv_dtype == 1) {
-    if (a.topk_idx) {
-      hipLaunchKernelGGL((attend_kernel<true, true>), dim3(workers), dim3(256), 0, s, a);
-    } else {
-      hipLaunchKernelGGL((attend_kernel<true, false>), dim3(workers), dim3(256), 0, s, a);
-    }
+    if (a.topk_idx) launch_attend_nt<true, true, false>(a, workers, s);
+    else launch_attend_nt<true, false, false>(a, workers, s);
   } else {
-    if (a.topk_idx) {
-      hipLaunchKernelGGL((attend_kernel<false, true>), dim3(workers), dim3(256), 0, s, a);
-    } else {
-      hipLaunchKernelGGL((attend_kernel<false, false>), dim3(workers), dim3(256), 0, s, a);
-    }
+    if (a.topk_idx) launch_attend_nt<false, true, false>(a, workers, s);
+    else launch_attend_nt<false, false, false>(a, workers, s);
   }
   return hipGetLastError();
 }
