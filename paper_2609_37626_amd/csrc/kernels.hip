@@ -1062,8 +1062,14 @@ void attend_kernel(AttendLaunch a) {
   const bool own_run = hdr[kHdrSchedule] == G;
   const int32_t run_begin = own_run ? hdr[kHdrWorkerTable + g] : 0;
   const int32_t run_end = own_run ? hdr[kHdrWorkerTable + g + 1] : hdr[kHdrUnits];
+  // With query chunks, the rows of one request read the same pages: the
+  // queue's neighbours (the longest-first order keeps a request's units
+  // together) go to workers of one XCD, whose L2 then serves the pages to
+  // all of them.  Workgroups are placed on the 8 XCDs round robin, so
+  // queue slot l of a pass goes to worker (l mod G/8) * 8 + l / (G/8).
+  const int32_t lg = (a.q_chunk > 1 && (G & 7) == 0) ? (g & 7) * (G >> 3) + (g >> 3) : g;
   auto unit_rec = [&](int k) -> i32x4 {
-    const int32_t u = own_run ? run_begin + k : k * G + ((k & 1) ? G - 1 - g : g);
+    const int32_t u = own_run ? run_begin + k : k * G + ((k & 1) ? G - 1 - lg : lg);
     if (u < run_end) return ((ConstI32x4*)a.ws.units)[u];
     return (i32x4){-1, 0, 0, 0};
   };
