@@ -565,9 +565,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
 // LDS layout of one staged step (32 cache rows): rows are cut into line
 // groups of 128 B (bf16) or 64 B (fp8); group g of row r sits at
 //   bf16: g*4096 + r*128 + ((c8 ^ ((r >> 1) & 7)) * 16)     (c8 = chunk in group)
-//   fp8:  g*2048 + r*64  + ((c4 ^ ((r >> 1) & 3)) * 16)
+//   fp8:  g*2048 + r*64  + ((c4 ^ swz4(r)) * 16),  swz4(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1)
 // so every 1 KB direct-to-LDS instruction reads whole memory lines of 8 (16)
-// rows, and the XOR spreads the operand reads over the LDS banks.
+// rows, and the XOR spreads the operand reads over the LDS banks.  (fp8: the
+// 16-byte slot of row r in a 256-byte bank period is 4 (r & 3) + (c4 ^
+// swz4(r)); with bit 3 of the row in the XOR, the 32 rows of a K-fragment
+// read fall two to a slot, the minimum, instead of four.)
 
 //
 // Latent rows (LAT: 656 B = 512 E4M3 codes at 0 | 4 fp32 tile scales at 512
@@ -575,6 +578,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
 // RoPE as one bf16 line group at kRopeOff, then the rows' tile scales (16 B
 // per row) at kData, and at kScaleT the same scales tile-major ([tile][row],
 // written by wave 0 once its loads landed).
+__device__ __forceinline__ uint32_t swz4(uint32_t r) { return ((r >> 1) & 3u) ^ ((r >> 3) & 1u); }
+
 template <bool FP8, bool LAT = false>
 struct StepLayout {
   static constexpr int kRowBytes = LAT ? 656 : FP8 ? kDimQK : 2 * kDimQK;   // 656 / 576 / 1152
@@ -1003,7 +1008,7 @@ void attend_kernel(AttendLaunch a) {
     dma_slot = 1024 * wave + 16 * lane;              // + 4096 t
   } else {
     dma_row = 16 * (wave & 1) + (lane >> 2);
-    src_lane = dma_row * L::kRowBytes + 64 * (wave >> 1) + (((lane & 3) ^ ((dma_row >> 1) & 3)) * 16);
+    src_lane = dma_row * L::kRowBytes + 64 * (wave >> 1) + (((lane & 3) ^ swz4(dma_row)) * 16);
     dma_slot = 2048 * (wave >> 1) + 1024 * (wave & 1) + 16 * lane;   // + 4096 t
   }
   // K operand of k-step ks (dims 16ks + 8h + [0, 8)): row n32, chunk
@@ -1017,7 +1022,7 @@ void attend_kernel(AttendLaunch a) {
     if constexpr (!FP8)
       kbase[m] = n32 * 128 + (((2 * m + h) ^ ((n32 >> 1) & 7)) * 16);
     else
-      kbase[m] = n32 * 64 + ((m ^ ((n32 >> 1) & 3)) * 16) + 8 * h;
+      kbase[m] = n32 * 64 + ((m ^ swz4(n32)) * 16) + 8 * h;
     kbase_r[m] = L::kRopeOff + n32 * 128 + (((2 * m + h) ^ ((n32 >> 1) & 7)) * 16);
   }
   // V operand (transposing reads), see load_v_frag
@@ -1042,7 +1047,7 @@ void attend_kernel(AttendLaunch a) {
 #pragma unroll
     for (int cbo = 0; cbo < 2; ++cbo) {
       const uint32_t c4 = 2 * cbo + (g16 & 1);
-      vbase[cbo][0] = rowk * 64 + ((c4 ^ ((rowk >> 1) & 3)) * 16) + 8 * (i16 & 1);
+      vbase[cbo][0] = rowk * 64 + ((c4 ^ swz4(rowk)) * 16) + 8 * (i16 & 1);  // rowk < 16: swz4 is that of rowk + 16
       vbase[cbo][1] = 0;
     }
   }

@@ -185,16 +185,4 @@ SPLASH_HD bool fold_applicable(int32_t T, int32_t G, int32_t max_workers, int32_
   return (int64_t)G * (busy + k.split_x16) < best_cost;
 }
 
-// ------------------------------------------------------------- LDS layout --
-//
-// A step stages 32 cache rows in LDS.  Rows keep their 16-byte chunks but the
-// chunk order inside each aligned group of 8 (bf16) or 4 (fp8) chunks is
-// XOR-permuted by row, so that the MFMA operand reads of 32 consecutive rows
-// spread over the LDS banks.
-SPLASH_HD uint32_t swz_bf16(uint32_t row) {
-  uint32_t g = ((row & 3u) << 1) | ((row >> 2) & 1u);
-  return g ^ (((row >> 3) & 1u) << 1);
-}
-SPLASH_HD uint32_t swz_fp8(uint32_t row) { return (row >> 1) & 3u; }
-
 }  // namespace splash
