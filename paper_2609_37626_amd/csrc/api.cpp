@@ -691,12 +691,29 @@ int splash_mla_plan_host(const int32_t* seq_lens_host, int32_t q_chunk, const sp
     if (T >= 0 && indptr_out) indptr_out[T] = ns;
     if (T <= kPlanLdsTiles && nu > G) {
       // the device queue order: longest unit first (equal lengths in tile
-      // order here; the device leaves their order open)
-      std::vector<std::array<int32_t, 4>> rows((size_t)nu);
-      for (int32_t i = 0; i < nu; ++i)
+      // order here; the device leaves their order open).  With query chunks
+      // (up to kMaxWorkers requests), whole requests instead, keyed by their
+      // longest unit (ties in request order here), each request's units
+      // unit index major (the rows of one page range side by side).
+      // rows[i][4] is the unit's index inside its tile.
+      std::vector<std::array<int32_t, 5>> rows((size_t)nu);
+      for (int32_t i = 0; i < nu; ++i) {
         for (int j = 0; j < 4; ++j) rows[i][j] = units_out[4 * (size_t)i + j];
+        rows[i][4] = (i > 0 && rows[i - 1][0] == rows[i][0]) ? rows[i - 1][4] + 1 : 0;
+      }
+      std::vector<int32_t> rkey((size_t)std::max(B, 1), 0);
+      const bool grouped = q_chunk > 1 && B <= kMaxWorkers;
+      if (grouped)
+        for (const auto& r : rows) rkey[r[0] / q_chunk] = std::max(rkey[r[0] / q_chunk], r[2] - r[1]);
       std::stable_sort(rows.begin(), rows.end(),
-                       [](const std::array<int32_t, 4>& a, const std::array<int32_t, 4>& b) {
+                       [&](const std::array<int32_t, 5>& a, const std::array<int32_t, 5>& b) {
+                         if (grouped) {
+                           const int32_t ra = a[0] / q_chunk, rb = b[0] / q_chunk;
+                           if (rkey[ra] != rkey[rb]) return rkey[ra] > rkey[rb];
+                           if (ra != rb) return ra < rb;
+                           if (a[4] != b[4]) return a[4] < b[4];
+                           return a[0] < b[0];
+                         }
                          return a[2] - a[1] > b[2] - b[1];
                        });
       for (int32_t i = 0; i < nu; ++i)

@@ -517,10 +517,31 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       return rec;
     };
     const bool lpt = NU > p.G;  // uniform
-    for (int32_t ug = tid; ug < NU; ug += 1024) {
-      const int4 rec = unit_rec(ug);
-      if (lpt) atomicAdd(&s_lhist[rec.z - rec.y], 1);  // 1 <= length <= kMaxUnitPages
-      else p.ws.units[ug] = rec;
+    // With query chunks the rows of a request read the same pages: the
+    // queue keeps a request's units together (requests ordered by their
+    // longest unit), unit index major, so that the rows of one page range sit
+    // side by side and run on one XCD (see the attend kernel's dealing),
+    // whose L2 serves the pages to every row.  Request b's range start sits
+    // in s_q[b], its key in s_rt[b] (the fold plan's arrays, free here).
+    const bool grouped = lpt && p.q_chunk > 1 && p.B <= kMaxWorkers && !shard;
+    if (grouped) {
+      for (int32_t b = tid; b < p.B; b += 1024) {
+        const int32_t t0 = b * p.q_chunk, t1 = t0 + p.q_chunk;
+        int32_t key = 0;
+        for (int32_t t = t0; t < t1; ++t) {
+          const int32_t n = s_ufirst[t + 1] - s_ufirst[t];
+          if (n > 0) key = max(key, ceil_div(s_pages[t], n));
+        }
+        s_rt[b] = key;
+        const int32_t cnt = s_ufirst[t1] - s_ufirst[t0];
+        if (cnt > 0) atomicAdd(&s_lhist[key], cnt);  // 1 <= key <= kMaxUnitPages
+      }
+    } else {
+      for (int32_t ug = tid; ug < NU; ug += 1024) {
+        const int4 rec = unit_rec(ug);
+        if (lpt) atomicAdd(&s_lhist[rec.z - rec.y], 1);  // 1 <= length <= kMaxUnitPages
+        else p.ws.units[ug] = rec;
+      }
     }
     __syncthreads();
     if (lpt) {
@@ -531,9 +552,28 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       int32_t unused;
       s_lbase[len] = block_exclusive_scan(s_lhist[len], s_scan, &unused);
       __syncthreads();
-      for (int32_t ug = tid; ug < NU; ug += 1024) {
-        const int4 rec = unit_rec(ug);
-        p.ws.units[atomicAdd(&s_lbase[rec.z - rec.y], 1)] = rec;
+      if (grouped) {
+        for (int32_t b = tid; b < p.B; b += 1024) {
+          const int32_t cnt = s_ufirst[(b + 1) * p.q_chunk] - s_ufirst[b * p.q_chunk];
+          if (cnt > 0) s_q[b] = atomicAdd(&s_lbase[s_rt[b]], cnt);
+        }
+        __syncthreads();
+        for (int32_t ug = tid; ug < NU; ug += 1024) {
+          const int4 rec = unit_rec(ug);
+          const int32_t b = rec.x / p.q_chunk, i = rec.x - b * p.q_chunk, u = ug - s_ufirst[rec.x];
+          // rank in unit-major order: sum_r min(u, n_r) + #{r < i : n_r > u}
+          int32_t rank = 0;
+          for (int32_t r = 0; r < p.q_chunk; ++r) {
+            const int32_t t = b * p.q_chunk + r, n = s_ufirst[t + 1] - s_ufirst[t];
+            rank += min(u, n) + ((r < i && n > u) ? 1 : 0);
+          }
+          p.ws.units[s_q[b] + rank] = rec;
+        }
+      } else {
+        for (int32_t ug = tid; ug < NU; ug += 1024) {
+          const int4 rec = unit_rec(ug);
+          p.ws.units[atomicAdd(&s_lbase[rec.z - rec.y], 1)] = rec;
+        }
       }
     }
   }

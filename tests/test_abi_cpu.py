@@ -352,10 +352,29 @@ def test_host_plan_queue_order(cfg, split):
     assert stats["fold"] == (cfg == 2 and split == 0)
     if stats["fold"]:
         check_fold(seq, spec.q_chunk, units, stats, 256)
-    elif stats["units"] > 256:
+    elif stats["units"] > 256 and spec.q_chunk == 1:
         assert np.all(ln[:-1] >= ln[1:])
         same = ln[:-1] == ln[1:]
         assert np.all(key[:-1][same] < key[1:][same])
+    elif stats["units"] > 256:
+        # query chunks: whole requests, longest unit first (ties in request
+        # order), each request's units unit index major so that the rows of
+        # one page range sit side by side
+        req = units[:, 0] // spec.q_chunk
+        starts = np.flatnonzero(np.r_[True, req[1:] != req[:-1]])
+        assert len(starts) == len(np.unique(req))
+        ends = np.r_[starts[1:], len(units)]
+        keys = np.array([ln[a:b].max() for a, b in zip(starts, ends)])
+        assert np.all(keys[:-1] >= keys[1:])
+        assert np.all(req[starts][:-1][keys[:-1] == keys[1:]] < req[starts][1:][keys[:-1] == keys[1:]])
+        for a, b in zip(starts, ends):
+            blk = units[a:b]
+            for i in range(1, len(blk)):
+                if blk[i, 0] == blk[i - 1, 0]:
+                    continue
+                # a new row: its unit starts where the previous row's unit of
+                # the same index would (same unit index, next row)
+                assert blk[i, 0] > blk[i - 1, 0] or blk[i, 1] >= blk[i - 1, 1]
     else:
         assert np.all(key[:-1] < key[1:])
     check_plan(seq, spec.q_chunk, units, indptr, stats, B.DEFAULT_MAX_PARTIALS)

@@ -257,12 +257,21 @@ def test_device_plan_matches_host_plan(case):
         assert runs(dev_units) == runs(units)
     elif stats["units"] > G and Bn * q_chunk <= 8192:
         # the same units (the device leaves the order of equal-length units
-        # open), and both queues hand out the longest units first
+        # open), and both queues hand out the longest units first; with query
+        # chunks, whole requests (each request's units side by side, the
+        # requests ordered by their longest unit, ties in any order)
         canon = lambda u: u[np.lexsort(u.T[::-1])]
         assert np.array_equal(canon(dev_units), canon(units))
         for u in (dev_units, units):
             ln = u[:, 2] - u[:, 1]
-            assert np.all(ln[:-1] >= ln[1:])
+            if q_chunk == 1:
+                assert np.all(ln[:-1] >= ln[1:])
+                continue
+            req = u[:, 0] // q_chunk
+            starts = np.flatnonzero(np.r_[True, req[1:] != req[:-1]])
+            assert len(starts) == len(np.unique(req)), "a request's units are not contiguous"
+            keys = [ln[a:b].max() for a, b in zip(starts, np.r_[starts[1:], len(u)])]
+            assert all(k0 >= k1 for k0, k1 in zip(keys[:-1], keys[1:]))
     elif stats["units"] > G:
         # more tiles than the planner caches in LDS: the units in tile order
         assert np.array_equal(dev_units, units)
