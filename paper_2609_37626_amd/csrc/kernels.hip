@@ -185,6 +185,41 @@ __device__ int32_t block_exclusive_scan(int32_t v, int32_t* wave_buf, int32_t* t
   return res;
 }
 
+// Three exclusive block scans at once (one set of barriers for the three).
+__device__ void block_exclusive_scan3(int32_t a, int32_t b, int32_t c, int32_t* wave_buf, int32_t* ea, int32_t* eb,
+                                      int32_t* ec, int32_t* ta, int32_t* tb, int32_t* tc) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t ia = wave_incl_scan(a), ib = wave_incl_scan(b), ic = wave_incl_scan(c);
+  if (lane == 63) {
+    wave_buf[wave] = ia;
+    wave_buf[17 + wave] = ib;
+    wave_buf[34 + wave] = ic;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int32_t xa = lane < 16 ? wave_buf[lane] : 0, xb = lane < 16 ? wave_buf[17 + lane] : 0,
+                  xc = lane < 16 ? wave_buf[34 + lane] : 0;
+    const int32_t ra = wave_incl_scan(xa), rb = wave_incl_scan(xb), rc = wave_incl_scan(xc);
+    if (lane < 16) {
+      wave_buf[lane] = ra - xa;
+      wave_buf[17 + lane] = rb - xb;
+      wave_buf[34 + lane] = rc - xc;
+    }
+    if (lane == 15) {
+      wave_buf[16] = ra;
+      wave_buf[33] = rb;
+      wave_buf[50] = rc;
+    }
+  }
+  __syncthreads();
+  *ea = wave_buf[wave] + ia - a;
+  *eb = wave_buf[17 + wave] + ib - b;
+  *ec = wave_buf[34 + wave] + ic - c;
+  *ta = wave_buf[16];
+  *tb = wave_buf[33];
+  *tc = wave_buf[50];
+  __syncthreads();
+}
 
 __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ int32_t s_pages[kPlanLdsTiles];
@@ -204,7 +239,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   __shared__ UDiv s_udiv[kNumCandidates + 1];      // their division magic
   __shared__ int32_t s_cand[kNumCandidates + 1];
   __shared__ int32_t s_parts[kNumCandidates];  // parts of each candidate
-  __shared__ int32_t s_scan[17];
+  __shared__ int32_t s_scan[51];
   __shared__ int32_t s_chunk;
   __shared__ int64_t s_best;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -293,12 +328,18 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
   const bool wide = nd > 64;
   const int nsl = wide ? 8 : 16;  // tile slices
   {
-    const int j = wide ? 64 * (wave >> 3) + lane : lane;
+    // With at most 32 sizes, 64 / np2 lanes share a size (np2: nd rounded up
+    // to a power of two), each taking every (64 / np2)-th tile of the slice;
+    // their sums meet by shuffles.  (uniform per wave)
+    const int np2 = wide ? 64 : (nd <= 1 ? 1 : 1 << (32 - __builtin_clz((unsigned)(nd - 1))));
+    const int sub = 64 / np2;
+    const int j = wide ? 64 * (wave >> 3) + lane : (lane & (np2 - 1));
+    const int part = wide ? 0 : lane / np2;
     const int slice = wide ? (wave & 7) : wave;
+    int64_t W = 0, S = 0;
     if (j < nd) {
       const int32_t ck = s_cand[s_list[j]];
       const UDiv ud = s_udiv[j];
-      int64_t W = 0, S = 0;
       auto count = [&](int32_t P) {
         const int32_t n = (int32_t)udiv((uint32_t)(P + ck - 1), ud);  // ceil(P / c)
         W += n;
@@ -306,10 +347,17 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
       };
       if (cached) {
 #pragma unroll 4
-        for (int32_t t = slice; t < T; t += nsl) count(s_pages[t]);
+        for (int32_t t = slice + nsl * part; t < T; t += nsl * sub) count(s_pages[t]);
       } else {
-        for (int32_t t = slice; t < T; t += nsl) count(dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end, p.topk_count));
+        for (int32_t t = slice + nsl * part; t < T; t += nsl * sub)
+          count(dev_tile_pages(p.seq_lens, p.q_chunk, t, p.key_begin, p.key_end, p.topk_count));
       }
+    }
+    for (int off = np2; off < 64; off <<= 1) {
+      W += __shfl_xor(W, off, 64);
+      S += __shfl_xor(S, off, 64);
+    }
+    if (j < nd && part == 0) {
       s_w[slice][j] = W;
       s_s[slice][j] = S;
     }
@@ -437,10 +485,11 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanLaunch p) {
     int32_t n = 0, sp = 0;
     if (t < T) tile_units(t, P, &n, &sp);
     const int32_t f = (sp > 0 || (list_empty && t < T && P == 0)) ? 1 : 0;
-    int32_t tu, ts, tf;
-    const int32_t eu = block_exclusive_scan(n, s_scan, &tu) + carry_u;
-    const int32_t es = block_exclusive_scan(sp, s_scan, &ts) + carry_s;
-    const int32_t ef = block_exclusive_scan(f, s_scan, &tf) + carry_f;
+    int32_t tu, ts, tf, eu, es, ef;
+    block_exclusive_scan3(n, sp, f, s_scan, &eu, &es, &ef, &tu, &ts, &tf);
+    eu += carry_u;
+    es += carry_s;
+    ef += carry_f;
     if (t < T) {
       if (cached) {
         s_ufirst[t] = eu;
