@@ -71,10 +71,10 @@ extern "C" {
  * little-endian fp32 scales (scale t covers latent columns [128t, 128t+128))
  * and the 64 RoPE values as bf16: K[d] = e4m3(code[d]) * scale[d / 128] for
  * d < 512, K[512 + r] = rope[r].  Scales must be positive normal powers
- * of two (the conversion uses only a scale's exponent); rows no history
- * reaches may hold anything.  Under SPLASH_FLAG_DEBUG_CHECK the whole-history
- * and shard entry points reject a reached row whose scale is not (the top-k
- * check validates lists and pages only).  kv_scales is ignored.
+ * of two no larger than 2^63 (the conversion uses only a scale's exponent,
+ * and the weights take it as an exponent step); rows no history reaches may
+ * hold anything.  Under SPLASH_FLAG_DEBUG_CHECK every entry point rejects a
+ * reached (top-k: listed) row whose scale is not.  kv_scales is ignored.
  * Every attend entry point (whole histories, shards, top-k) and the gather
  * take it. */
 #define SPLASH_KV_FP8_LATENT 2

@@ -959,30 +959,38 @@ __device__ __forceinline__ bf16x8 fp8x8_scaled_to_bf16(u32x2 raw, float scale) {
 
 // Latent rows: a wave's PV covers output columns [128 wave, +128), one
 // latent tile, so the tile scale of each key multiplies that key's P weight
-// instead of V.  s[e] is the scale of the key of fragment element e.
-__device__ __forceinline__ bf16x8 scale_p(bf16x8 p, const float (&s)[8]) {
+// instead of V.  The scales are powers of two 2^e, so the product is the
+// weight with e added to its bf16 exponent field: one packed 16-bit add per
+// pair of weights (d holds e << 7 of both keys), and a packed max that
+// turns an exponent pushed below the normal range into 0.  Exact while the
+// result stays normal: weights are at most 2^64 in the pass that is kept
+// and e <= 63 (a scale above 2^63 is outside the format); a weight pushed
+// below 2^-126 contributes nothing the fp32 sum would keep.
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bf16x8 scale_p(bf16x8 p, const u32x4& d) {
   const u32x4 w = __builtin_bit_cast(u32x4, p);
   u32x4 r;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    r[i] = pack_bf16x2(__builtin_bit_cast(float, w[i] << 16) * s[2 * i],
-                       __builtin_bit_cast(float, w[i] & 0xffff0000u) * s[2 * i + 1]);
+  for (int i = 0; i < 4; ++i) {
+    // (scalar copies first: a bit cast taken straight from a vector element
+    // reads element 0 whatever the index)
+    const unsigned wi = w[i], di = d[i];
+    const u16x2 sum = __builtin_bit_cast(u16x2, wi) + __builtin_bit_cast(u16x2, di);
+    r[i] = __builtin_bit_cast(unsigned, __builtin_elementwise_max(__builtin_bit_cast(i16x2, sum), (i16x2){0, 0}));
+  }
   return __builtin_bit_cast(bf16x8, r);
 }
 
-// Latent rows: the tile-`wave` scales of the 8 keys of the P^T fragment
-// (key half kh) a lane reads; element e is key 16kh + 8(e >> 2) + 4h + (e & 3)
-// (the slot order of the P exchange).  scales_t: the tile-major copy, so the
-// two runs of 4 keys are two 16-byte reads.
-__device__ __forceinline__ void load_p_scales(const uint8_t LDS_AS* scales_t, int kh, int h, int wave,
-                                              float (&s)[8]) {
-  const uint8_t LDS_AS* base = scales_t + 4 * (32 * wave + 16 * kh + 4 * h);
-  const f32x4 a = *(const f32x4 LDS_AS*)base, b = *(const f32x4 LDS_AS*)(base + 32);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    s[e] = a[e];
-    s[4 + e] = b[e];
-  }
+// Latent rows: the exponent steps (e << 7, 16 bits per key) of the tile-`wave`
+// scales of the 8 keys of the P^T fragment (key half kh) a lane reads;
+// element e is key 16kh + 8(e >> 2) + 4h + (e & 3) (the slot order of the P
+// exchange), so the four key pairs are two 8-byte reads of the tile-major
+// table ([tile][key], 2 bytes each).
+__device__ __forceinline__ void load_p_scales(const uint8_t LDS_AS* scales_t, int kh, int h, int wave, u32x4& d) {
+  const uint8_t LDS_AS* base = scales_t + 2 * (32 * wave + 16 * kh + 4 * h);
+  const u32x2 a = *(const u32x2 LDS_AS*)base, b = *(const u32x2 LDS_AS*)(base + 16);
+  d = (u32x4){a[0], a[1], b[0], b[1]};
 }
 
 // P^T operand fragment (head block hb, key half kh) from the P exchange area:
@@ -1006,7 +1014,7 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
   for (int hb = 4 - kPVDefer; hb < 4; ++hb) o[3][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dv, dp[hb], o[3][hb], 0, 0, 0);
   // V fragments are double-buffered one column block ahead (c = 4kh + cbl).
   bf16x8 pf[4], vf[2];
-  float psc[8];
+  u32x4 psc;
   if constexpr (LAT) load_p_scales(vbuf + lat_scales, 0, h, wave, psc);
 #pragma unroll
   for (int hb = 0; hb < 4; ++hb) {
@@ -1366,11 +1374,15 @@ void attend_kernel(AttendLaunch a) {
           }
         }
         if constexpr (LAT) {
-          // the tile-major copy of the step's scales (after the zero fill)
+          // the tile-major table of the step's scale exponents (after the
+          // zero fill): (bits >> 16) - (127 << 7) is e << 7 for 2^e; a
+          // zeroed scale (rows past the end, whose weights are 0) gives a
+          // step that keeps those weights 0
           if (wave == 0 && lane < 32) {
-            const f32x4 v = *(const f32x4 LDS_AS*)(buf + L::kData + 16 * lane);
+            const u32x4 v = *(const u32x4 LDS_AS*)(buf + L::kData + 16 * lane);
 #pragma unroll
-            for (int t = 0; t < 4; ++t) *(float LDS_AS*)(buf + L::kScaleT + 4 * (32 * t + lane)) = v[t];
+            for (int t = 0; t < 4; ++t)
+              *(uint16_t LDS_AS*)(buf + L::kScaleT + 2 * (32 * t + lane)) = (uint16_t)(((v[t] >> 16) & 0x7F80u) - 0x3F80u);
           }
         }
         // step j staged; P of step j-1 visible; every wave is done with
@@ -1384,7 +1396,7 @@ void attend_kernel(AttendLaunch a) {
         // 32 - kPV1 PV MFMAs run under the softmax (stream 2).
         f32x16 sacc;
         bf16x8 pf[4], pf1[4];
-        float psc[2][8];  // LAT: tile-`wave` scales of the keys of pf / pf1
+        u32x4 psc[2];  // LAT: tile-`wave` scale exponent steps of the keys of pf / pf1
         FragRaw<FP8> vf[3];  // V fragments of three column blocks, as read
         bf16x8 vcur;         // that of the current column block, converted
         {
@@ -2017,7 +2029,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint8_t* kv, const in
 // Writes the smallest failing request + 1 (or 0).
 // latent_kv (the fp8 latent-row pool, else null): once every page entry of a
 // request is in range, each of its rows' four tile scales must be a positive
-// normal power of two.
+// normal power of two no larger than 2^63.
 __global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int32_t* seq_lens,
                                                     const int32_t* key_begin, const int32_t* key_end, int32_t B,
                                                     int32_t q_chunk, int32_t bt_stride, int32_t num_pages,
@@ -2045,7 +2057,7 @@ __global__ __launch_bounds__(256) void check_kernel(const int32_t* bt, const int
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const uint32_t e = (sc[t] >> 23) & 0xFF;
-          if ((sc[t] & 0x807FFFFFu) != 0 || e == 0 || e == 0xFF) bad = true;
+          if ((sc[t] & 0x807FFFFFu) != 0 || e == 0 || e > 127 + 63) bad = true;
         }
       }
     }
@@ -2058,7 +2070,8 @@ __global__ void init_check(int32_t* result) { *result = INT32_MAX; }
 // Top-k variant: every row's count in [0, topk], every used position in the
 // row's visible prefix [0, s_b - q_chunk + i], and its page's block-table
 // entry in [0, num_pages); with the fp8 latent-row pool (latent_kv non-null)
-// also each listed row's four tile scales a positive normal power of two.
+// also each listed row's four tile scales a positive normal power of two
+// no larger than 2^63.
 // Writes the smallest failing row + 1 (or 0).
 __global__ __launch_bounds__(256) void topk_check_kernel(const int32_t* bt, const int32_t* seq_lens,
                                                          const int32_t* idx, const int32_t* count, int32_t N,
@@ -2085,7 +2098,7 @@ __global__ __launch_bounds__(256) void topk_check_kernel(const int32_t* bt, cons
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
               const uint32_t ex = (sc[t] >> 23) & 0xFF;
-              if ((sc[t] & 0x807FFFFFu) != 0 || ex == 0 || ex == 0xFF) bad = true;
+              if ((sc[t] & 0x807FFFFFu) != 0 || ex == 0 || ex > 127 + 63) bad = true;
             }
           }
         }

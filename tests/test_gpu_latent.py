@@ -108,11 +108,16 @@ def test_debug_check_rejects_scales_that_are_not_powers_of_two():
     out_dbg, lse_dbg = gpu_attend(batch, flags=B.FLAG_DEBUG_CHECK)   # valid data passes, same result
     assert torch.equal(out_ref.view(torch.int16), out_dbg.view(torch.int16)) and torch.equal(lse_ref, lse_dbg)
     p0, p1 = int(batch.block_table[0, 2]), int(batch.block_table[1, 0])
-    for page, row, value in [(p0, 1, 3.0), (p1, 63, -0.5), (p0, 0, 0.0), (p0, 1, np.inf)]:
+    # (the weights take a scale as an exponent step, so the format also caps
+    # scales at 2^63)
+    for page, row, value in [(p0, 1, 3.0), (p1, 63, -0.5), (p0, 0, 0.0), (p0, 1, np.inf), (p1, 2, 2.0 ** 64)]:
         kv = batch.kv.copy()
         kv[page, row, 512 + 4:512 + 8] = np.array([value], dtype='<f4').view(np.uint8)   # tile 1
         with pytest.raises(B.SplashError):
             gpu_attend(dataclasses.replace(batch, kv=kv), flags=B.FLAG_DEBUG_CHECK)
+    kv = batch.kv.copy()
+    kv[p1, 2, 512 + 4:512 + 8] = np.array([2.0 ** 63], dtype='<f4').view(np.uint8)    # the largest allowed
+    gpu_attend(dataclasses.replace(batch, kv=kv), flags=B.FLAG_DEBUG_CHECK)
     # a row past the end of history 0 (130 keys: page 2 holds keys 128, 129)
     # is never reached, so its scales may hold anything
     kv = batch.kv.copy()
@@ -158,7 +163,7 @@ def test_topk_debug_check_rejects_listed_scales_that_are_not_powers_of_two():
     def row_of(b, pos):
         return int(batch.block_table[b, pos // 64]), pos % 64
 
-    for (b, pos), value in [((0, 130), 3.0), ((1, 199), -0.5), ((0, 5), 0.0), ((1, 0), np.inf)]:
+    for (b, pos), value in [((0, 130), 3.0), ((1, 199), -0.5), ((0, 5), 0.0), ((1, 0), np.inf), ((0, 299), 2.0 ** 64)]:
         page, r = row_of(b, pos)
         kv = batch.kv.copy()
         kv[page, r, 512 + 8:512 + 12] = np.array([value], dtype='<f4').view(np.uint8)   # tile 2
