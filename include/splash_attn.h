@@ -106,9 +106,9 @@ typedef struct splash_mla_desc {
 
 /*
  * Workspace.  One caller-allocated device buffer carries the plan (work list,
- * split offsets) and the fp32 partial results of split histories.
+ * split offsets) and the partial results of split histories.
  * `max_partials` bounds how many partial results (one per work unit of a
- * split history, H x 512 fp32 each) the planner may use; <= 0 selects
+ * split history, room for H x 512 fp32 each) the planner may use; <= 0 selects
  * SPLASH_DEFAULT_MAX_PARTIALS.  The planner never exceeds the capacity that
  * the passed ws_bytes provides: with too little room it splits less.
  * Layout (byte offsets from splash_mla_workspace_offsets, 256-byte aligned):
@@ -125,7 +125,13 @@ typedef struct splash_mla_desc {
  *       [off[t], off[t+1]); empty when the tile is a single unit)
  *   [3] split tiles int32[B*q_chunk] (the tiles with partials, ascending)
  *   [4] partial lse fp32 [max_partials, H]
- *   [5] partial out fp32 [max_partials, H, 512]
+ *   [5] partial out: room for fp32 [max_partials, H, 512]; the library keeps
+ *       them as fp16 [max_partials, H, 512] (the first half of the region),
+ *       each (slot, head) 128-column quarter q multiplied by 2^-e, with e
+ *       byte q of uint32 [max_partials, H] right after them (e = 0 unless
+ *       the quarter's largest magnitude reaches 2^15; then every stored
+ *       value stays below 2^15).  Internal: only splash_mla_combine_splits
+ *       reads them.
  */
 #define SPLASH_DEFAULT_MAX_PARTIALS 1024
 size_t splash_mla_workspace_size(int32_t batch, int32_t q_chunk, int32_t num_heads,
@@ -198,8 +204,8 @@ int splash_mla_run(const void* q, const void* kv_pages, const int32_t* block_tab
  * splash_mla_attend_units + splash_mla_combine_splits: splash_mla_run in its
  * two launches.  attend_units processes every work unit of the plan: a tile
  * (query row with all heads) that is one unit writes its out/lse rows
- * directly; the units of a split tile write fp32 partials into the
- * workspace.  combine_splits merges those partials into out/lse (its
+ * directly; the units of a split tile write partials (fp16 with a
+ * power-of-two scale, see the workspace layout) into the workspace.  combine_splits merges those partials into out/lse (its
  * arguments must match the attend_units call).  Same argument rules as
  * splash_mla_run.
  */

@@ -85,6 +85,10 @@ Workspace workspace_view(void* ws, int64_t T, int32_t H, int64_t max_partials) {
   w.split_list = reinterpret_cast<int4*>(base + L.off[3]);
   w.part_lse = reinterpret_cast<float*>(base + L.off[4]);
   w.part_out = reinterpret_cast<float*>(base + L.off[5]);
+  // the split partials in fp16 fill the first half of the region; the
+  // quarter exponents follow them
+  w.part_half = reinterpret_cast<uint16_t*>(base + L.off[5]);
+  w.part_exp = reinterpret_cast<uint32_t*>(base + L.off[5] + sizeof(uint16_t) * (size_t)max_partials * H * kDimV);
   w.max_units = (int32_t)(T + max_partials);
   w.max_partials = (int32_t)max_partials;
   return w;
@@ -237,7 +241,9 @@ int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_ta
 int do_combine_splits(int32_t q_chunk, void* out, float* lse, const splash_mla_desc* d, const Workspace& wv,
                       hipStream_t s, const Shard& sh = Shard()) {
   CombineLaunch c;
-  c.partials = wv.part_out;
+  c.partials = nullptr;
+  c.partials_h = wv.part_half;
+  c.part_exp = wv.part_exp;
   c.partial_lse = wv.part_lse;
   c.indptr = wv.indptr;
   c.item_list = wv.split_list;
@@ -537,6 +543,8 @@ int splash_mla_combine(const float* partials, const float* partial_lse, const in
     return fail(SPLASH_ERR_MISALIGNED, "partials and out must be 16-byte aligned");
   CombineLaunch c;
   c.partials = partials;
+  c.partials_h = nullptr;
+  c.part_exp = nullptr;
   c.partial_lse = partial_lse;
   c.indptr = split_indptr;
   c.item_list = nullptr;

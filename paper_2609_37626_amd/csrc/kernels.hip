@@ -90,6 +90,29 @@ __device__ __forceinline__ unsigned pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(unsigned, v);
 }
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ unsigned pack_f16x2(float a, float b) {
+  f16x2 v = __builtin_convertvector((f32x2){a, b}, f16x2);
+  return __builtin_bit_cast(unsigned, v);
+}
+
+// Split partials are stored in fp16, each (slot, head) quarter of 128
+// columns multiplied by 2^-e: e = 0 unless the quarter's largest magnitude
+// m reaches 2^15, else e = floor(log2 m) - 14, so every stored value stays
+// below 2^15 and rescales exactly.  The exponent of magnitude m is read from
+// its bits (a zero m gives e = 0; e <= 114).
+__device__ __forceinline__ uint32_t partial_exponent(float m) {
+  const int32_t ex = (int32_t)((__builtin_bit_cast(uint32_t, m) >> 23) & 255u) - 127 - 14;
+  return ex > 0 ? (uint32_t)ex : 0u;
+}
+// Four stored fp16 values (two dwords) back to fp32, times 2^e.
+__device__ __forceinline__ f32x4 unpack_f16x4(uint32_t lo, uint32_t hi, int e) {
+  const f32x2 a = __builtin_convertvector(__builtin_bit_cast(f16x2, lo), f32x2);
+  const f32x2 b = __builtin_convertvector(__builtin_bit_cast(f16x2, hi), f32x2);
+  return (f32x4){__builtin_amdgcn_ldexpf(a[0], e), __builtin_amdgcn_ldexpf(a[1], e), __builtin_amdgcn_ldexpf(b[0], e),
+                 __builtin_amdgcn_ldexpf(b[1], e)};
+}
+
 // 8 E4M3 codes (two dwords) -> 8 bf16 (exact).
 __device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 raw) {
   u32x4 r;
@@ -1074,7 +1097,9 @@ void attend_kernel(AttendLaunch a) {
   constexpr int kBtOff = kPOff + 2 * kPBytes;
   constexpr int kStageRow = 128 * 4 + 16;            // epilogue: bytes per head, padded off the banks
   constexpr int kLOff = 4 * 32 * kStageRow;          // epilogue: per-head normaliser, 128 floats
-  constexpr int kStageBytes = kLOff + kMaxHeads * 4;
+  constexpr int kScOff = kLOff + kMaxHeads * 4;      // epilogue: per wave, the normalisers times each
+                                                     // head's quarter scale (split partials)
+  constexpr int kStageBytes = kScOff + 4 * kMaxHeads * 4;
   constexpr int kStageOff = (kOverlap && FP8) ? kBtOff : 0;
   constexpr int kSlotBase = (kOverlap && !FP8) ? 2 : 0;
   static_assert(!(kOverlap && !FP8) || kStageBytes <= 2 * L::kBuf, "bf16 staging fits in ring slots 0-1");
@@ -1716,7 +1741,7 @@ void attend_kernel(AttendLaunch a) {
     __syncthreads();
     // Each head block goes through LDS (the ring is free: every wave is past
     // its last PV and no load is in flight), so that the stores write whole
-    // rows (512 B of fp32 or 256 B of bf16 per head) instead of the
+    // rows (256 B of fp16 or bf16 per head) instead of the
     // accumulators' 32-byte pieces spread over 32 rows.  NT: the stores are
     // non-temporal too.  Lines left dirty in the L2 are written back at the
     // kernel's end, after the last worker; streamed stores shorten that
@@ -1739,9 +1764,12 @@ void attend_kernel(AttendLaunch a) {
         // stored: as H is a multiple of 16, the rows of head block hb to
         // store are k < (H - 32 hb) / 2, a multiple of 8, the same for the
         // whole wave.
+        // (a split partial: this wave's normalisers, times each quarter's scale)
+        const float LDS_AS* l_rows =
+            slot >= 0 ? (const float LDS_AS*)(sm + kStageOff + kScOff) + kMaxHeads * wave : l_lds;
         f32x4 rl[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) rl[i] = *(const f32x4 LDS_AS*)(l_lds + 32 * hb + 16 * hl + 4 * i);
+        for (int i = 0; i < 4; ++i) rl[i] = *(const f32x4 LDS_AS*)(l_rows + 32 * hb + 16 * hl + 4 * i);
         const int kval = min(16, (a.H - 32 * hb) / 2);
 #pragma unroll 1
         for (int k0 = 0; k0 < kval; k0 += 8) {
@@ -1768,6 +1796,33 @@ void attend_kernel(AttendLaunch a) {
           for (int q = 0; q < 4; ++q)
             *(f32x4 LDS_AS*)(stage + (32 * cbl + 8 * q) * 4) =
                 (f32x4){o[cbl][hb][4 * q], o[cbl][hb][4 * q + 1], o[cbl][hb][4 * q + 2], o[cbl][hb][4 * q + 3]};
+        if (slot >= 0) {
+          // split partial: the largest magnitude of the lane's 64 columns,
+          // read back from the staged copy (through a laundered address, so
+          // that the compiler does not keep the accumulator values for it)
+          const uint8_t LDS_AS* rb =
+              sm + opaque((uint32_t)(kStageOff + wave * 32 * kStageRow + nl * kStageRow + 16 * hl));
+          float m = 0.f;
+#pragma unroll
+          for (int cbl = 0; cbl < 4; ++cbl)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const f32x4 x = *(const f32x4 LDS_AS*)(rb + (32 * cbl + 8 * q) * 4);
+              m = fmaxf(m, fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3]))));
+            }
+          // the quarter's scale: lanes n32 and n32 + 32 hold head 32 hb + n32's
+          // 128 columns of this wave; the scale goes to this wave's table at
+          // the normaliser's index (read back below by the lanes that store
+          // the head's rows), its exponent to byte `wave` of the head's word
+          m = fmaxf(m, wave_xor32(m));
+          const int li = 32 * hb + 16 * (nl & 1) + (nl >> 1);
+          const float rcp = l_lds[li];
+          const uint32_t e = partial_exponent(m * rcp);
+          if (hl == 0) {
+            ((float LDS_AS*)(sm + kStageOff + kScOff))[kMaxHeads * wave + li] = rcp * __builtin_bit_cast(float, (127u - e) << 23);
+            if (32 * hb + nl < a.H) ((uint8_t*)(a.ws.part_exp + (size_t)slot * a.H + 32 * hb + nl))[wave] = (uint8_t)e;
+          }
+        }
         if (slot < 0) {
           uint16_t* obase = (uint16_t*)a.out + (size_t)tile * a.H * kDimV + col;
           rows(hb, [&](int hh, const f32x4& v) {
@@ -1778,10 +1833,13 @@ void attend_kernel(AttendLaunch a) {
             else *(u32x2*)(obase + (size_t)hh * kDimV) = w;
           });
         } else {
-          float* pbase = a.ws.part_out + (size_t)slot * a.H * kDimV + col;
+          uint16_t* pbase = a.ws.part_half + (size_t)slot * a.H * kDimV + col;
           rows(hb, [&](int hh, const f32x4& v) {
-            if constexpr (NT) __builtin_nontemporal_store(v, (f32x4*)(pbase + (size_t)hh * kDimV));
-            else *(f32x4*)(pbase + (size_t)hh * kDimV) = v;
+            u32x2 w;
+            w[0] = pack_f16x2(v[0], v[1]);
+            w[1] = pack_f16x2(v[2], v[3]);
+            if constexpr (NT) __builtin_nontemporal_store(w, (u32x2*)(pbase + (size_t)hh * kDimV));
+            else *(u32x2*)(pbase + (size_t)hh * kDimV) = w;
           });
         }
       }
@@ -1824,18 +1882,43 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
     const size_t base = (size_t)qi * c.H + hh;
     const size_t orow = out_row(b, qi) * c.H + hh;
     const float* plse = c.partial_lse + base;
-    const float* prow = c.partials + base * kDimV + 8 * lane;
     f32x4 v[kCombineRowParts][2];
     float w[kCombineRowParts];
+    if (c.partials_h) {
+      // fp16 partials: the lane's 8 columns lie in quarter lane / 16
+      const uint16_t* prow = c.partials_h + base * kDimV + 8 * lane;
+      const uint32_t* pexp = c.part_exp + base;
+      u32x4 raw[kCombineRowParts];
+      uint32_t ew[kCombineRowParts];
 #pragma unroll
-    for (int u = 0; u < kCombineRowParts; ++u) {
-      w[u] = -INFINITY;
-      v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
-      if (u < np) {  // uniform
-        w[u] = plse[(size_t)(s0 + u) * stride];
-        const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
-        v[u][0] = src[0];
-        v[u][1] = src[1];
+      for (int u = 0; u < kCombineRowParts; ++u) {
+        w[u] = -INFINITY;
+        raw[u] = (u32x4){0, 0, 0, 0};
+        ew[u] = 0;
+        if (u < np) {  // uniform
+          w[u] = plse[(size_t)(s0 + u) * stride];
+          raw[u] = *(const u32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
+          ew[u] = pexp[(size_t)(s0 + u) * stride];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kCombineRowParts; ++u) {
+        const int e = (int)((ew[u] >> (8 * (lane >> 4))) & 255u);
+        v[u][0] = unpack_f16x4(raw[u][0], raw[u][1], e);
+        v[u][1] = unpack_f16x4(raw[u][2], raw[u][3], e);
+      }
+    } else {
+      const float* prow = c.partials + base * kDimV + 8 * lane;
+#pragma unroll
+      for (int u = 0; u < kCombineRowParts; ++u) {
+        w[u] = -INFINITY;
+        v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        if (u < np) {  // uniform
+          w[u] = plse[(size_t)(s0 + u) * stride];
+          const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
+          v[u][0] = src[0];
+          v[u][1] = src[1];
+        }
       }
     }
     float M = -INFINITY, wsum = 0.f;
@@ -1878,6 +1961,108 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
     }
     return;
   }
+  if (c.item_list && c.partials_h) {
+    // The attend kernel's fp16 partials, some item with more parts than
+    // that: one workgroup per (item, row, head), each lane 8 columns of the
+    // row.  Wave w takes parts w, w + 4, ..., eight in flight, and keeps a
+    // running maximum of their LSEs (its sums rescaled when it grows), so
+    // each batch costs one round trip to memory; the four waves' (maximum,
+    // weight sum, column sums) meet in LDS, where wave 0 merges them.
+    __shared__ f32x4 s_acc[4][64][2];
+    __shared__ float s_ms[4][2];
+    const int w = threadIdx.x >> 6;
+    const int qsh = 8 * (lane >> 4);  // the lane's columns lie in quarter lane / 16
+    const int64_t per_item = (int64_t)c.q_chunk * c.H;
+    for (int64_t item = blockIdx.x; item < nreq * per_item; item += gridDim.x) {
+      const int64_t ri = item / per_item;
+      const int row = (int)(item - ri * per_item);
+      const int qi = row / c.H, hh = row - qi * c.H;
+      const int4 rec = c.item_list[ri];
+      const int s0 = rec.y, np = rec.z;
+      const size_t base = (size_t)qi * c.H + hh;
+      const float* plse = c.partial_lse + base;
+      const uint16_t* prow = c.partials_h + base * kDimV + 8 * lane;
+      float m = -INFINITY, ssum = 0.f;
+      f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+      constexpr int kU = 8;
+      for (int u0 = w; u0 < np; u0 += 4 * kU) {
+        u32x4 raw[kU];
+        float wu[kU];
+        uint32_t ew[kU];
+#pragma unroll
+        for (int k = 0; k < kU; ++k) {
+          const int u = u0 + 4 * k;
+          raw[k] = (u32x4){0, 0, 0, 0};
+          wu[k] = -INFINITY;
+          ew[k] = 0;
+          if (u < np) {  // uniform
+            const size_t r = (size_t)(s0 + u) * stride;
+            raw[k] = *(const u32x4*)(prow + r * kDimV);
+            wu[k] = plse[r];
+            ew[k] = c.part_exp[r + base];
+          }
+        }
+        float bm = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < kU; ++k) bm = fmaxf(bm, wu[k]);
+        if (bm > -INFINITY) {  // uniform
+          const float mn = fmaxf(m, bm), rs = __expf(m - mn);  // 0 while m is -inf
+          acc0 *= rs;
+          acc1 *= rs;
+          ssum *= rs;
+          m = mn;
+#pragma unroll
+          for (int k = 0; k < kU; ++k) {
+            const int e = (int)((ew[k] >> qsh) & 255u);
+            const float sc = __expf(wu[k] - m);  // 0 for parts past the end
+            ssum += sc;
+            acc0 += sc * unpack_f16x4(raw[k][0], raw[k][1], e);
+            acc1 += sc * unpack_f16x4(raw[k][2], raw[k][3], e);
+          }
+        }
+      }
+      s_acc[w][lane][0] = acc0;
+      s_acc[w][lane][1] = acc1;
+      if (lane == 0) {
+        s_ms[w][0] = m;
+        s_ms[w][1] = ssum;
+      }
+      __syncthreads();
+      if (w == 0) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) M = fmaxf(M, s_ms[v][0]);
+        float wsum = 0.f;
+        acc0 = acc1 = (f32x4){0.f, 0.f, 0.f, 0.f};
+        if (M > -INFINITY) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float f = __expf(s_ms[v][0] - M);  // 0 for a wave without parts
+            wsum += f * s_ms[v][1];
+            acc0 += f * s_acc[v][lane][0];
+            acc1 += f * s_acc[v][lane][1];
+          }
+        }
+        const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+        const size_t orow = out_row(rec.x, qi) * c.H + hh;
+        if (c.out_f32) {
+          f32x4* dst = (f32x4*)((float*)c.out + orow * kDimV + 8 * lane);
+          dst[0] = acc0 * inv;
+          dst[1] = acc1 * inv;
+        } else {
+          u32x4 o4;
+          o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
+          o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
+          o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
+          o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
+          *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
+        }
+        if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+      }
+      __syncthreads();  // s_acc and s_ms are free for the next item
+    }
+    return;
+  }
   // one (request or tile, row, head, quarter) item
   auto combine_item = [&](int b, int s0, int s1, int quarter, int qi, int hh) {
     const size_t orow = out_row(b, qi) * c.H + hh;
@@ -1885,13 +2070,15 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
     const size_t base = (size_t)qi * c.H + hh;
     const float* plse = c.partial_lse + base;
     const int col = 128 * quarter + 2 * lane;
+    // the lane's 2 columns of part s (fp32 partials: this path serves the
+    // standalone merge)
+    auto part2 = [&](int sp) -> f32x2 { return *(const f32x2*)(c.partials + ((size_t)sp * stride + base) * kDimV + col); };
     float M = -INFINITY, wsum = 0.f;
     f32x2 acc = {0.f, 0.f};
     if (nparts <= 8) {
       // few parts: every lane loads every part's LSE itself (the same 32
       // bytes for the whole wave) together with its 2 columns of every part,
       // so the row costs one round trip to memory and no cross-lane reduction
-      const float* prow = c.partials + base * kDimV + col;
       f32x2 v[8];
       float w[8];
 #pragma unroll
@@ -1900,7 +2087,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
         v[u] = (f32x2){0.f, 0.f};
         if (u < nparts) {  // uniform
           w[u] = plse[(size_t)(s0 + u) * stride];
-          v[u] = *(const f32x2*)(prow + (size_t)(s0 + u) * stride * kDimV);
+          v[u] = part2(s0 + u);
         }
       }
 #pragma unroll
@@ -1921,7 +2108,6 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
       wsum = __ockl_wfred_add_f32(wsum);
       // many parts: sixteen parts' columns in flight at a time
       if (M > -INFINITY) {
-        const float* prow = c.partials + base * kDimV + col;
         constexpr int kU = 16;
         int s = s0;
         for (; s + kU <= s1; s += kU) {
@@ -1929,7 +2115,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
           float w[kU];
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
-            v[u] = *(const f32x2*)(prow + (size_t)(s + u) * stride * kDimV);
+            v[u] = part2(s + u);
             w[u] = plse[(size_t)(s + u) * stride];
           }
 #pragma unroll
@@ -1942,7 +2128,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
             const int su = s + u < s1 ? s + u : s1 - 1;
-            v[u] = *(const f32x2*)(prow + (size_t)su * stride * kDimV);
+            v[u] = part2(su);
             w[u] = s + u < s1 ? plse[(size_t)su * stride] : -INFINITY;
           }
 #pragma unroll

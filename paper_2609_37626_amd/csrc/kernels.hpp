@@ -14,7 +14,9 @@ struct Workspace {
   int32_t* indptr;      // [T + 1]
   int4* split_list;     // [T] {tile, first partial slot, parts, 0} of the tiles with partials (count in the header)
   float* part_lse;      // [max_partials, H]
-  float* part_out;      // [max_partials, H, 512]
+  float* part_out;      // region of [max_partials, H, 512] floats, which holds the split partials as
+  uint16_t* part_half;  //   fp16 [max_partials, H, 512] (its first half), each (slot, head) 128-column
+  uint32_t* part_exp;   //   quarter q scaled by 2^-e with e = byte q of part_exp[slot * H + head]
   int32_t max_units;
   int32_t max_partials;
 };
@@ -65,7 +67,9 @@ struct AttendLaunch {
 };
 
 struct CombineLaunch {
-  const float* partials;
+  const float* partials;      // fp32 partials (the standalone merge), or
+  const uint16_t* partials_h; // the attend kernel's fp16 partials with their quarter exponents
+  const uint32_t* part_exp;
   const float* partial_lse;
   const int32_t* indptr;     // [B + 1] partial-slot offsets (per request or per tile)
   const int4* item_list;     // optional {request, first slot, parts, 0} records to process (count from

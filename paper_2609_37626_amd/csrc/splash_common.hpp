@@ -32,7 +32,7 @@ constexpr int kPlanLdsTiles = 8192;  // planner: tile data cached in LDS, and th
 // A tile is one query row n = b*q_chunk + i with all H heads; it sees
 // L = s_b - q_chunk + i + 1 keys (its complete causal prefix), i.e.
 // ceil(L/64) pages.  The planner cuts each tile's page range into units of at
-// most c pages; a tile cut into more than one unit writes fp32 partials that
+// most c pages; a tile cut into more than one unit writes partials that
 // the combine step merges.  c is chosen by an argmin of an estimated step
 // time over candidate sizes.  The G persistent workers are dealt the units of
 // a queue, so with W units the busiest worker runs R = ceil(W / G) of them: the

@@ -4,6 +4,7 @@ Tolerances (the parity bar): outputs max-abs 1e-2 for bf16 caches and 3e-2
 for the fp8 cache, LSE max-abs 1e-3; page resolution and run-to-run results
 bit-exact.
 """
+import dataclasses
 import os
 
 import numpy as np
@@ -102,6 +103,31 @@ def test_forced_splits_and_combine(split_pages):
     ref = run_oracle(batch)
     out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=split_pages)
     assert_parity(batch, out, lse, *ref, label=f"forced split {split_pages}")
+
+
+def scale_bf16_bits(bits, k):
+    """Multiply bf16 values (bit patterns) by 2^k exactly: k added to the
+    exponent field of every nonzero value (all normal here, none overflows)."""
+    b = bits.astype(np.int32)
+    nz = (b & 0x7FFF) != 0
+    assert np.all(((b[nz] >> 7) & 0xFF) + k > 0) and np.all(((b[nz] >> 7) & 0xFF) + k < 255)
+    return np.where(nz, b + (k << 7), b).astype(np.uint16)
+
+
+@pytest.mark.parametrize("split_pages", [3, 40])
+def test_split_partials_beyond_fp16_range(split_pages):
+    """Split partials are kept in fp16 with a power-of-two scale per (slot,
+    head, 128 columns).  With the cache times 2^17 and the query times 2^-17
+    the scores are unchanged and every output is exactly 2^17 times the
+    unscaled one, up to |out| ~ 2^19, far past fp16's 65504: the scaled run
+    divided by 2^17 must meet the bar against the unscaled oracle (an
+    unscaled fp16 partial would be infinite)."""
+    base = W.make_custom([9000, 13001, 65], H=128, seed=21)
+    ref_out, ref_lse = run_oracle(base)
+    batch = dataclasses.replace(base, q=scale_bf16_bits(base.q, -17), kv=scale_bf16_bits(base.kv, 17))
+    out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=split_pages)
+    assert float(out.float().abs().max()) > 65504.0
+    assert_parity(base, out.float() * 2.0 ** -17, lse, ref_out, ref_lse, label=f"fp16 range, split {split_pages}")
 
 
 def test_forced_splits_fp8_chunk():
