@@ -1854,18 +1854,16 @@ void attend_kernel(AttendLaunch a) {
 constexpr int kCombineQuarters = 4;  // waves per (row, head): 128 columns each
 constexpr int kCombineRowParts = 8;  // at most this many parts: one wave per (row, head)
 //
-// Four wave slots per (request or tile, chunk row, head), 128 columns each
-// (2 per lane).  With at most 8 parts every lane loads all parts' LSEs and
-// its columns of all parts at once; with more, the LSEs are reduced across
-// the lanes first and sixteen parts' columns are in flight at a time.
+// The standalone merge of fp32 partials by split offsets (splash_mla_combine).
+// Four wave slots per (request, chunk row, head), 128 columns each (2 per
+// lane).  With at most 8 parts every lane loads all parts' LSEs and its
+// columns of all parts at once; with more, the LSEs are reduced across the
+// lanes first and sixteen parts' columns are in flight at a time.
 __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
   const int lane = threadIdx.x & 63;
   const int64_t wave_global = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  const int64_t per_req = (int64_t)c.q_chunk * c.H * kCombineQuarters;
-  const int64_t nreq = c.item_list ? (int64_t)(*c.item_count) : (int64_t)c.B;
-  const int64_t total = nreq * per_req;
-  if (total == 0) return;
+  if (c.B <= 0) return;
   const size_t stride = (size_t)c.q_chunk * c.H;  // between parts
   // output row of (item b, chunk row qi): b * q_chunk + qi, or its place
   // among the shards
@@ -1884,41 +1882,16 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
     const float* plse = c.partial_lse + base;
     f32x4 v[kCombineRowParts][2];
     float w[kCombineRowParts];
-    if (c.partials_h) {
-      // fp16 partials: the lane's 8 columns lie in quarter lane / 16
-      const uint16_t* prow = c.partials_h + base * kDimV + 8 * lane;
-      const uint32_t* pexp = c.part_exp + base;
-      u32x4 raw[kCombineRowParts];
-      uint32_t ew[kCombineRowParts];
+    const float* prow = c.partials + base * kDimV + 8 * lane;
 #pragma unroll
-      for (int u = 0; u < kCombineRowParts; ++u) {
-        w[u] = -INFINITY;
-        raw[u] = (u32x4){0, 0, 0, 0};
-        ew[u] = 0;
-        if (u < np) {  // uniform
-          w[u] = plse[(size_t)(s0 + u) * stride];
-          raw[u] = *(const u32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
-          ew[u] = pexp[(size_t)(s0 + u) * stride];
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kCombineRowParts; ++u) {
-        const int e = (int)((ew[u] >> (8 * (lane >> 4))) & 255u);
-        v[u][0] = unpack_f16x4(raw[u][0], raw[u][1], e);
-        v[u][1] = unpack_f16x4(raw[u][2], raw[u][3], e);
-      }
-    } else {
-      const float* prow = c.partials + base * kDimV + 8 * lane;
-#pragma unroll
-      for (int u = 0; u < kCombineRowParts; ++u) {
-        w[u] = -INFINITY;
-        v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        if (u < np) {  // uniform
-          w[u] = plse[(size_t)(s0 + u) * stride];
-          const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
-          v[u][0] = src[0];
-          v[u][1] = src[1];
-        }
+    for (int u = 0; u < kCombineRowParts; ++u) {
+      w[u] = -INFINITY;
+      v[u][0] = v[u][1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      if (u < np) {  // uniform
+        w[u] = plse[(size_t)(s0 + u) * stride];
+        const f32x4* src = (const f32x4*)(prow + (size_t)(s0 + u) * stride * kDimV);
+        v[u][0] = src[0];
+        v[u][1] = src[1];
       }
     }
     float M = -INFINITY, wsum = 0.f;
@@ -1949,120 +1922,6 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
     }
     if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
   };
-  if (c.item_list && c.max_parts && *c.max_parts <= kCombineRowParts) {
-    // every listed item has at most kCombineRowParts parts
-    const int64_t per_item = (int64_t)c.q_chunk * c.H;
-    for (int64_t item = wave_global; item < nreq * per_item; item += nwaves) {
-      const int64_t ri = item / per_item;
-      const int row = (int)(item - ri * per_item);
-      const int qi = row / c.H, hh = row - qi * c.H;
-      const int4 rec = c.item_list[ri];
-      row_merge(rec.x, rec.y, rec.z, qi, hh);
-    }
-    return;
-  }
-  if (c.item_list && c.partials_h) {
-    // The attend kernel's fp16 partials, some item with more parts than
-    // that: one workgroup per (item, row, head), each lane 8 columns of the
-    // row.  Wave w takes parts w, w + 4, ..., eight in flight, and keeps a
-    // running maximum of their LSEs (its sums rescaled when it grows), so
-    // each batch costs one round trip to memory; the four waves' (maximum,
-    // weight sum, column sums) meet in LDS, where wave 0 merges them.
-    __shared__ f32x4 s_acc[4][64][2];
-    __shared__ float s_ms[4][2];
-    const int w = threadIdx.x >> 6;
-    const int qsh = 8 * (lane >> 4);  // the lane's columns lie in quarter lane / 16
-    const int64_t per_item = (int64_t)c.q_chunk * c.H;
-    for (int64_t item = blockIdx.x; item < nreq * per_item; item += gridDim.x) {
-      const int64_t ri = item / per_item;
-      const int row = (int)(item - ri * per_item);
-      const int qi = row / c.H, hh = row - qi * c.H;
-      const int4 rec = c.item_list[ri];
-      const int s0 = rec.y, np = rec.z;
-      const size_t base = (size_t)qi * c.H + hh;
-      const float* plse = c.partial_lse + base;
-      const uint16_t* prow = c.partials_h + base * kDimV + 8 * lane;
-      float m = -INFINITY, ssum = 0.f;
-      f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-      constexpr int kU = 8;
-      for (int u0 = w; u0 < np; u0 += 4 * kU) {
-        u32x4 raw[kU];
-        float wu[kU];
-        uint32_t ew[kU];
-#pragma unroll
-        for (int k = 0; k < kU; ++k) {
-          const int u = u0 + 4 * k;
-          raw[k] = (u32x4){0, 0, 0, 0};
-          wu[k] = -INFINITY;
-          ew[k] = 0;
-          if (u < np) {  // uniform
-            const size_t r = (size_t)(s0 + u) * stride;
-            raw[k] = *(const u32x4*)(prow + r * kDimV);
-            wu[k] = plse[r];
-            ew[k] = c.part_exp[r + base];
-          }
-        }
-        float bm = -INFINITY;
-#pragma unroll
-        for (int k = 0; k < kU; ++k) bm = fmaxf(bm, wu[k]);
-        if (bm > -INFINITY) {  // uniform
-          const float mn = fmaxf(m, bm), rs = __expf(m - mn);  // 0 while m is -inf
-          acc0 *= rs;
-          acc1 *= rs;
-          ssum *= rs;
-          m = mn;
-#pragma unroll
-          for (int k = 0; k < kU; ++k) {
-            const int e = (int)((ew[k] >> qsh) & 255u);
-            const float sc = __expf(wu[k] - m);  // 0 for parts past the end
-            ssum += sc;
-            acc0 += sc * unpack_f16x4(raw[k][0], raw[k][1], e);
-            acc1 += sc * unpack_f16x4(raw[k][2], raw[k][3], e);
-          }
-        }
-      }
-      s_acc[w][lane][0] = acc0;
-      s_acc[w][lane][1] = acc1;
-      if (lane == 0) {
-        s_ms[w][0] = m;
-        s_ms[w][1] = ssum;
-      }
-      __syncthreads();
-      if (w == 0) {
-        float M = -INFINITY;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) M = fmaxf(M, s_ms[v][0]);
-        float wsum = 0.f;
-        acc0 = acc1 = (f32x4){0.f, 0.f, 0.f, 0.f};
-        if (M > -INFINITY) {
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const float f = __expf(s_ms[v][0] - M);  // 0 for a wave without parts
-            wsum += f * s_ms[v][1];
-            acc0 += f * s_acc[v][lane][0];
-            acc1 += f * s_acc[v][lane][1];
-          }
-        }
-        const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-        const size_t orow = out_row(rec.x, qi) * c.H + hh;
-        if (c.out_f32) {
-          f32x4* dst = (f32x4*)((float*)c.out + orow * kDimV + 8 * lane);
-          dst[0] = acc0 * inv;
-          dst[1] = acc1 * inv;
-        } else {
-          u32x4 o4;
-          o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
-          o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
-          o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
-          o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
-          *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
-        }
-        if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
-      }
-      __syncthreads();  // s_acc and s_ms are free for the next item
-    }
-    return;
-  }
   // one (request or tile, row, head, quarter) item
   auto combine_item = [&](int b, int s0, int s1, int quarter, int qi, int hh) {
     const size_t orow = out_row(b, qi) * c.H + hh;
@@ -2143,10 +2002,10 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
       *(unsigned*)((uint16_t*)c.out + orow * kDimV + col) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     if (lane == 0 && quarter == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
   };
-  if (!c.item_list) {
-    // by indptr (the standalone merge): one wave per (request, row, head),
-    // which takes the one-round-trip row merge when the request has at most
-    // kCombineRowParts parts and otherwise the four quarters in turn
+  {
+    // one wave per (request, row, head), which takes the one-round-trip row
+    // merge when the request has at most kCombineRowParts parts and
+    // otherwise the four quarters in turn
     const int64_t per_b = (int64_t)c.q_chunk * c.H;
     for (int64_t item = wave_global; item < (int64_t)c.B * per_b; item += nwaves) {
       const int b = (int)(item / per_b);
@@ -2160,29 +2019,142 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
         for (int quarter = 0; quarter < kCombineQuarters; ++quarter) combine_item(b, s0, s1, quarter, qi, hh);
       }
     }
+  }
+}
+
+// The merge of one step's split partials (splash_mla_combine_splits): the
+// attend kernel's fp16 partials with their quarter exponents, the split
+// tiles listed by the planner.  Every (tile, chunk row, head) row is one
+// item; a lane holds 8 of its 512 columns (quarter lane / 16).  With at most
+// kMergeWaveParts parts per tile (the plan's bound) a wave takes an item
+// alone; with more, a workgroup takes it and its four waves split the
+// parts.  Either way parts go kMergeBatch at a time, one memory round trip
+// per batch, against a running maximum of their LSEs (the sums rescaled
+// when it grows); the four waves of a workgroup meet in LDS.  Few registers,
+// so that many waves hide the round trips.
+constexpr int kMergeWaveParts = 4;
+constexpr int kMergeBatch = 4;
+__global__ __launch_bounds__(256) void merge_splits_kernel(CombineLaunch c) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t nitems = (int64_t)(*c.item_count) * c.q_chunk * c.H;
+  if (nitems == 0) return;
+  const bool by_wave = *c.max_parts <= kMergeWaveParts;  // uniform
+  const size_t stride = (size_t)c.q_chunk * c.H;          // between parts
+  const int qsh = 8 * (lane >> 4);
+  // parts first, first + step, ... of an item: running max m, weight sum,
+  // column sums
+  auto accumulate = [&](const int4& rec, size_t base, int first, int step, float& m, float& ssum, f32x4& acc0,
+                        f32x4& acc1) {
+    const int s0 = rec.y, np = rec.z;
+    const float* plse = c.partial_lse + base;
+    const uint16_t* prow = c.partials_h + base * kDimV + 8 * lane;
+    for (int u0 = first; u0 < np; u0 += step * kMergeBatch) {
+      u32x4 raw[kMergeBatch];
+      float wu[kMergeBatch];
+      uint32_t ew[kMergeBatch];
+#pragma unroll
+      for (int k = 0; k < kMergeBatch; ++k) {
+        const int u = u0 + step * k;
+        raw[k] = (u32x4){0, 0, 0, 0};
+        wu[k] = -INFINITY;
+        ew[k] = 0;
+        if (u < np) {  // uniform
+          const size_t r = (size_t)(s0 + u) * stride;
+          raw[k] = *(const u32x4*)(prow + r * kDimV);
+          wu[k] = plse[r];
+          ew[k] = c.part_exp[r + base];
+        }
+      }
+      float bm = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < kMergeBatch; ++k) bm = fmaxf(bm, wu[k]);
+      if (bm > -INFINITY) {  // uniform
+        const float mn = fmaxf(m, bm), rs = __expf(m - mn);  // 0 while m is -inf
+        acc0 *= rs;
+        acc1 *= rs;
+        ssum *= rs;
+        m = mn;
+#pragma unroll
+        for (int k = 0; k < kMergeBatch; ++k) {
+          const int e = (int)((ew[k] >> qsh) & 255u);
+          const float sc = __expf(wu[k] - m);  // 0 for parts past the end
+          ssum += sc;
+          acc0 += sc * unpack_f16x4(raw[k][0], raw[k][1], e);
+          acc1 += sc * unpack_f16x4(raw[k][2], raw[k][3], e);
+        }
+      }
+    }
+  };
+  auto store = [&](const int4& rec, int qi, int hh, float M, float wsum, const f32x4& acc0, const f32x4& acc1) {
+    size_t r = (size_t)rec.x * c.q_chunk + qi;
+    if (c.num_shards > 0) {
+      const size_t rb = r / (size_t)c.tile_q, ri = r - rb * (size_t)c.tile_q;
+      r = (rb * c.num_shards + c.shard) * c.tile_q + ri;
+    }
+    const size_t orow = r * c.H + hh;
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    if (c.out_f32) {
+      f32x4* dst = (f32x4*)((float*)c.out + orow * kDimV + 8 * lane);
+      dst[0] = acc0 * inv;
+      dst[1] = acc1 * inv;
+    } else {
+      u32x4 o4;
+      o4[0] = pack_bf16x2(acc0[0] * inv, acc0[1] * inv);
+      o4[1] = pack_bf16x2(acc0[2] * inv, acc0[3] * inv);
+      o4[2] = pack_bf16x2(acc1[0] * inv, acc1[1] * inv);
+      o4[3] = pack_bf16x2(acc1[2] * inv, acc1[3] * inv);
+      *(u32x4*)((uint16_t*)c.out + orow * kDimV + 8 * lane) = o4;
+    }
+    if (lane == 0 && c.out_lse) c.out_lse[orow] = wsum > 0.f ? M + __logf(wsum) : -INFINITY;
+  };
+  const int64_t per_tile = (int64_t)c.q_chunk * c.H;
+  if (by_wave) {
+    const int64_t nwaves = (int64_t)gridDim.x * 4;
+    for (int64_t item = (int64_t)blockIdx.x * 4 + w; item < nitems; item += nwaves) {
+      const int64_t ri = item / per_tile;
+      const int row = (int)(item - ri * per_tile), qi = row / c.H, hh = row - qi * c.H;
+      const int4 rec = c.item_list[ri];
+      float m = -INFINITY, ssum = 0.f;
+      f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+      accumulate(rec, (size_t)qi * c.H + hh, 0, 1, m, ssum, acc0, acc1);
+      store(rec, qi, hh, m, ssum, acc0, acc1);
+    }
     return;
   }
-  for (int64_t item = wave_global; item < total; item += nwaves) {
-    const int64_t ri = item / per_req;
-    const int rem = (int)(item - ri * per_req);
-    const int quarter = rem & (kCombineQuarters - 1);
-    const int row = rem / kCombineQuarters;
-    const int qi = row / c.H, hh = row - qi * c.H;
-    // the request (or tile) and its part range: one record, or two reads of
-    // indptr
-    int b, s0, s1;
-    if (c.item_list) {
-      const int4 rec = c.item_list[ri];
-      b = rec.x;
-      s0 = rec.y;
-      s1 = rec.y + rec.z;
-    } else {
-      b = (int)ri;
-      s0 = c.indptr[b];
-      s1 = c.indptr[b + 1];
+  __shared__ f32x4 s_acc[4][64][2];
+  __shared__ float s_ms[4][2];
+  for (int64_t item = blockIdx.x; item < nitems; item += gridDim.x) {
+    const int64_t ri = item / per_tile;
+    const int row = (int)(item - ri * per_tile), qi = row / c.H, hh = row - qi * c.H;
+    const int4 rec = c.item_list[ri];
+    float m = -INFINITY, ssum = 0.f;
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    accumulate(rec, (size_t)qi * c.H + hh, w, 4, m, ssum, acc0, acc1);
+    s_acc[w][lane][0] = acc0;
+    s_acc[w][lane][1] = acc1;
+    if (lane == 0) {
+      s_ms[w][0] = m;
+      s_ms[w][1] = ssum;
     }
-    if (s1 <= s0 && !c.write_empty) continue;
-    combine_item(b, s0, s1, quarter, qi, hh);
+    __syncthreads();
+    if (w == 0) {
+      float M = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) M = fmaxf(M, s_ms[v][0]);
+      float wsum = 0.f;
+      acc0 = acc1 = (f32x4){0.f, 0.f, 0.f, 0.f};
+      if (M > -INFINITY) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float f = __expf(s_ms[v][0] - M);  // 0 for a wave without parts
+          wsum += f * s_ms[v][1];
+          acc0 += f * s_acc[v][lane][0];
+          acc1 += f * s_acc[v][lane][1];
+        }
+      }
+      store(rec, qi, hh, M, wsum, acc0, acc1);
+    }
+    __syncthreads();  // s_acc and s_ms are free for the next item
   }
 }
 
@@ -2326,6 +2298,15 @@ hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) 
 }
 
 hipError_t launch_combine(const CombineLaunch& c, hipStream_t s) {
+  if (c.item_list) {
+    // the step's split tiles (their number is on the device): a block per
+    // (tile, row, head) up to the bound, the kernel strides over the rest
+    int64_t blocks = (int64_t)c.B * c.q_chunk * c.H;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(merge_splits_kernel, dim3((unsigned)blocks), dim3(256), 0, s, c);
+    return hipGetLastError();
+  }
   int64_t items = (int64_t)c.B * c.q_chunk * c.H * kCombineQuarters;
   int64_t blocks = (items + 3) / 4;
   if (blocks > 4096) blocks = 4096;
