@@ -2026,19 +2026,25 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineLaunch c) {
 // attend kernel's fp16 partials with their quarter exponents, the split
 // tiles listed by the planner.  Every (tile, chunk row, head) row is one
 // item; a lane holds 8 of its 512 columns (quarter lane / 16).  With at most
-// kMergeWaveParts parts per tile (the plan's bound) a wave takes an item
-// alone; with more, a workgroup takes it and its four waves split the
-// parts.  Either way parts go kMergeBatch at a time, one memory round trip
-// per batch, against a running maximum of their LSEs (the sums rescaled
-// when it grows); the four waves of a workgroup meet in LDS.  Few registers,
-// so that many waves hide the round trips.
+// kMergeWaveParts parts per tile (the plan's bound), or with at least
+// kMergeWaveItems items of at most kMergeWaveLongParts parts (items enough
+// to fill the chip with waves, so a workgroup per item would only queue
+// them), a wave takes an item alone; otherwise a workgroup takes it and its
+// four waves split the parts.  Either way parts go kMergeBatch at a time,
+// one memory round trip per batch, against a running maximum of their LSEs
+// (the sums rescaled when it grows); the four waves of a workgroup meet in
+// LDS.  Few registers, so that many waves hide the round trips.
 constexpr int kMergeWaveParts = 4;
+constexpr int kMergeWaveItems = 8192;
+constexpr int kMergeWaveLongParts = 16;
 constexpr int kMergeBatch = 4;
 __global__ __launch_bounds__(256) void merge_splits_kernel(CombineLaunch c) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t nitems = (int64_t)(*c.item_count) * c.q_chunk * c.H;
   if (nitems == 0) return;
-  const bool by_wave = *c.max_parts <= kMergeWaveParts;  // uniform
+  const int max_parts = *c.max_parts;
+  const bool by_wave = max_parts <= kMergeWaveParts ||
+                       (nitems >= kMergeWaveItems && max_parts <= kMergeWaveLongParts);  // uniform
   const size_t stride = (size_t)c.q_chunk * c.H;          // between parts
   const int qsh = 8 * (lane >> 4);
   // parts first, first + step, ... of an item: running max m, weight sum,
