@@ -130,6 +130,16 @@ def test_split_partials_beyond_fp16_range(split_pages):
     assert_parity(base, out.float() * 2.0 ** -17, lse, ref_out, ref_lse, label=f"fp16 range, split {split_pages}")
 
 
+def test_many_split_rows_with_several_parts_each():
+    """The step's merge takes each (split tile, head) on one wave when there
+    are at least 8,192 of them with at most 16 parts each, in several
+    batches of four parts: 9 requests x 8 chunk rows = 72 split tiles, x 128
+    heads = 9,216 rows, 5 or 6 parts per tile."""
+    batch = W.make_custom([610, 640, 700, 655, 620, 690, 600, 680, 645], H=128, q_chunk=8, seed=24)
+    out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=2)
+    assert_parity(batch, out, lse, label="merge by wave, 5-6 parts")
+
+
 def test_forced_splits_fp8_chunk():
     batch = W.make_custom([700, 2000], H=128, q_chunk=8, kv_dtype=W.KV_FP8_E4M3, seed=22)
     out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=4)
