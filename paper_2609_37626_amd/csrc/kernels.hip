@@ -4,8 +4,10 @@
 //
 // Attend kernel design (one persistent workgroup per compute unit):
 //  * Work unit = (query row n with all H heads, page range).  Under a fold
-//    plan each worker runs its own run of units; otherwise units come from a
-//    device queue filled by the planner, drawn with one atomic.
+//    plan each worker runs its own run of units; otherwise the planner's
+//    queue (longest unit first) is dealt to the workers in a snake.  Neither
+//    takes an atomic, so a worker knows its next unit ahead and issues that
+//    unit's query and first steps before its current epilogue.
 //  * 4 waves, one per SIMD.  For QK^T and the softmax wave w owns heads
 //    [32w, 32w+32), whose query rows stay in VGPRs for the whole unit (36
 //    16-byte MFMA B fragments); for PV it owns output columns [128w, +128)
@@ -32,6 +34,10 @@
 //  * O^T[512 x heads] += V^T P^T on MFMA: P^T fragments come from the P
 //    exchange area in LDS and V^T is read from the same staged rows with
 //    ds_read_b64_tr_b16 (bf16) or ds_read_b64_tr_b8 (fp8) transposing loads.
+//  * Epilogue: O/l goes through LDS so that every store writes whole rows;
+//    an unsplit tile stores bf16 out and its LSE, a split unit an fp16
+//    partial with a power-of-two scale per 128 columns and its LSE, which
+//    merge_splits_kernel folds into the tile's result.
 //  * fp8 cache: E4M3 codes convert exactly to bf16; the per-token scale is
 //    applied in fp32 to the score and to P before P is rounded for PV.
 //  * fp8 latent-row cache (656-byte rows: E4M3 latent with a power-of-two

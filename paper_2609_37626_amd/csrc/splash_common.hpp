@@ -20,7 +20,7 @@ constexpr int kDimV = 512;         // d_z = d_c
 constexpr int kLatentRowBytes = 656;  // fp8 latent-row cache: 512 E4M3 + 4 fp32 tile scales + 64 bf16 RoPE
 constexpr int kMaxHeads = 128;
 constexpr int kStepKeys = 32;      // keys per pipeline step (half a page)
-constexpr int kMaxUnitPages = 1024;  // the block-table slice of one unit is staged in LDS
+constexpr int kMaxUnitPages = 1024;  // the largest unit: the planner's length histograms and fold caps count to it
 constexpr int kTopkUnitPages = 32;   // top-k variant: a unit holds 32 x 64 selected rows' addresses in LDS
 constexpr int kMaxWorkers = 1024;    // the fold plan's per-worker table is sized for this many
 constexpr int kHeaderInts = 1152;    // 64 header slots, then the per-worker table (kMaxWorkers + 1)
