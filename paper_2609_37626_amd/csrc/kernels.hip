@@ -131,6 +131,56 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 raw) {
 
 __device__ __forceinline__ float wave_xor32(float v) { return __shfl_xor(v, 32, 64); }
 
+// ---- QK^T of the per-token fp8 cache on the fp8 matrix pipe.  A bf16
+// query value has 8 significant bits and an E4M3 code 4, so after scaling a
+// head's row by a power of two that puts its largest |q| in [128, 256), each
+// value x is the sum of two codes: hi = rne(x), then lo = rne(x - hi), whose
+// residual has at most 4 significant bits.  The split is exact for |x| >=
+// 1/4 (2^-10 of the row's largest value); below that the residual's lowest
+// bits fall under E4M3's smallest subnormal 2^-9, and each such term is off
+// by at most 2^-10, 2^-17 of the largest.  K enters as the cache's own codes.  S = scale * (K hi^T + K lo^T),
+// two 32x32x64 MFMAs per 64 dims, with no per-step conversion of K.
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+// 32 bf16 values of one 64-dim block (16 dwords: values 0-15 in `a`, 16-31
+// in `b`, two per dword, low half first) times `inv` -> hi codes into `a`,
+// lo codes into `b` (value v at byte v % 4 of dword v / 4).
+__device__ __forceinline__ void split_query_block(i32x8& a, i32x8& b, float inv) {
+  i32x8 hi, lo;
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    const uint32_t d0 = (uint32_t)(g < 4 ? a[2 * g] : b[2 * g - 8]);
+    const uint32_t d1 = (uint32_t)(g < 4 ? a[2 * g + 1] : b[2 * g - 7]);
+    const float x0 = __uint_as_float(d0 << 16) * inv, x1 = __uint_as_float(d0 & 0xFFFF0000u) * inv;
+    const float x2 = __uint_as_float(d1 << 16) * inv, x3 = __uint_as_float(d1 & 0xFFFF0000u) * inv;
+    s16x2 w = {0, 0};
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, x0, x1, 1.0f, false);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, x2, x3, 1.0f, true);
+    const int hw = __builtin_bit_cast(int, w);
+    const f32x2 h01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(hw, 1.0f, false);
+    const f32x2 h23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(hw, 1.0f, true);
+    s16x2 v = {0, 0};
+    v = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(v, x0 - h01[0], x1 - h01[1], 1.0f, false);
+    v = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(v, x2 - h23[0], x3 - h23[1], 1.0f, true);
+    hi[g] = hw;
+    lo[g] = __builtin_bit_cast(int, v);
+  }
+  a = hi;
+  b = lo;
+}
+
+// One 32x32x64 fp8 MFMA of the QK^T chain (VGPR accumulator, as mfma_qk).
+// K comes straight from LDS and the query codes were written at the unit's
+// start, so no VALU result feeds it.
+template <bool FIRST>
+__device__ __forceinline__ void mfma_qk8(f32x16& acc, const i32x8& k, const i32x8& q) {
+  if constexpr (FIRST)
+    asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, 0" : "=v"(acc) : "v"(k), "v"(q));
+  else
+    asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, %0" : "+v"(acc) : "v"(k), "v"(q));
+}
+
 // ============================================================== planner ===
 
 // Pages of tile t: its whole causal prefix, or under a shard its keys in
@@ -1122,6 +1172,10 @@ void attend_kernel(AttendLaunch a) {
   const int head = 32 * wave + n32;
   const bool head_ok = head < a.H;
   const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
+  // per-token fp8 cache: QK on the fp8 matrix pipe with the query split in
+  // two E4M3 terms; its power-of-two row scale joins the softmax constant
+  constexpr bool kQ8 = FP8 && !LAT;
+  float c2v = c2;
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
   uint8_t LDS_AS* p_lds = sm + kPOff;
@@ -1236,11 +1290,42 @@ void attend_kernel(AttendLaunch a) {
   // Padding heads (head >= H) take head 0's row: their scores stay finite and
   // nothing of theirs is stored.  (Nothing consumes the loaded values here,
   // so the loads stay in flight until the first QK MFMA.)
-  bf16x8 qf[36];
+  // (kQ8: fragments 2m and 2m + 1 side by side in q8[m]; after
+  // split_query, q8[2kb] holds the hi codes of dims block kb, q8[2kb + 1] the
+  // lo codes, in the byte order of the fp8 K operand)
+  bf16x8 qf[kQ8 ? 1 : 36];
+  i32x8 q8[kQ8 ? 18 : 1];
   auto load_q = [&](int t) {
     const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)t * a.H + (head_ok ? head : 0)) * kDimQK + 8 * h;
+    if constexpr (kQ8) {
 #pragma unroll
-    for (int ks = 0; ks < 36; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + 16 * ks));
+      for (int m = 0; m < 18; ++m) {
+        const u32x4 f0 = *(const u32x4*)(qrow + 32 * m), f1 = *(const u32x4*)(qrow + 32 * m + 16);
+        q8[m] = __builtin_bit_cast(i32x8, __builtin_shufflevector(f0, f1, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < 36; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + 16 * ks));
+    }
+  };
+  // kQ8: the head's row scale (lanes l and l ^ 32 hold its two halves), then
+  // the split of every block; sets the lane's softmax constant
+  auto split_query = [&]() {
+    float mx = 0.f;
+#pragma unroll
+    for (int m = 0; m < 18; ++m)
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        const uint32_t w = (uint32_t)q8[m][d];
+        mx = fmaxf(mx, fmaxf(fabsf(__uint_as_float(w << 16)), fabsf(__uint_as_float(w & 0xFFFF0000u))));
+      }
+    mx = fmaxf(mx, wave_xor32(mx));
+    int e = (int)((__float_as_uint(mx) >> 23) & 255u) - 127;  // floor(log2 max), -127 for 0
+    e = e < -100 ? -100 : (e > 120 ? 120 : e);
+    const float inv = __uint_as_float((uint32_t)(127 + 7 - e) << 23);  // 2^(7 - e)
+    c2v = c2 * __uint_as_float((uint32_t)(127 - 7 + e) << 23);         // c2 * 2^(e - 7)
+#pragma unroll
+    for (int kb = 0; kb < 9; ++kb) split_query_block(q8[2 * kb], q8[2 * kb + 1], inv);
   };
 
   i32x4 cur = unit_rec(0), nxt = unit_rec(1);
@@ -1330,6 +1415,9 @@ void attend_kernel(AttendLaunch a) {
             issue_step<FP8, LAT, NT>(step_src(j, ph), step_scales(j, ph), src_lane, slot_buf(j), wave);
           }
         }
+      if constexpr (kQ8) {
+        if (pass == 0) split_query();
+      }
 
 #pragma unroll
       for (int x = 0; x < 4; ++x)
@@ -1432,13 +1520,27 @@ void attend_kernel(AttendLaunch a) {
         bf16x8 vcur;         // that of the current column block, converted
         {
           constexpr int kKPre = 4;  // K fragments in flight
-          FragRaw<FP8> kf[kKPre];
+          FragRaw<FP8> kf[kQ8 ? 1 : kKPre];
+          // kQ8: K operands of dims blocks kb in a ring of three, each read a
+          // block ahead, so a block's registers are rewritten five slots
+          // (two 64-cycle MFMAs) after their last MFMA was issued
+          i32x8 k8[kQ8 ? 3 : 1];
+          auto load_k8 = [&](int kb) {
+            const u32x2 r0 = load_k_raw<true>(buf, kbase, 4 * kb), r1 = load_k_raw<true>(buf, kbase, 4 * kb + 1);
+            const u32x2 r2 = load_k_raw<true>(buf, kbase, 4 * kb + 2), r3 = load_k_raw<true>(buf, kbase, 4 * kb + 3);
+            const u32x4 lo4 = __builtin_shufflevector(r0, r1, 0, 1, 2, 3), hi4 = __builtin_shufflevector(r2, r3, 0, 1, 2, 3);
+            return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+          };
           bf16x8 ka_prev;  // fp8: the converted fragment the previous QK MFMA was issued with
           bf16x8 kr[4];    // LAT: the RoPE fragments, bf16 as staged
           f32x4 tsc;       // LAT: tile scales of this lane's key row
           if constexpr (LAT) tsc = *(const f32x4 LDS_AS*)(buf + L::kData + 16 * n32);
+          if constexpr (kQ8) {
+            k8[0] = load_k8(0);
+          } else {
 #pragma unroll
-          for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_raw<FP8>(buf, kbase, ks);
+            for (int ks = 0; ks < kKPre; ++ks) kf[ks] = load_k_raw<FP8>(buf, kbase, ks);
+          }
           if constexpr (kPV) {
             // the MFMAs step j-2 deferred, operands in registers, while the
             // first K fragments arrive
@@ -1466,22 +1568,34 @@ void attend_kernel(AttendLaunch a) {
               const int cn = (q >> 2) + 2;
               vf[cn % 3] = load_v_raw<FP8>(vbuf, vbase, 4 * wave + (cn & 3), cn >> 2);
             }
-            bf16x8 ka;
-            if constexpr (LAT) ka = i < 32 ? fp8x8_scaled_to_bf16(kf[i % kKPre], tsc[i >> 3]) : kr[i & 3];
-            else ka = frag_bf16<FP8>(kf[i % kKPre]);
-            if constexpr (FP8) {
-              // the conversion must not reuse the registers of the MFMA just
-              // issued (the asm hides that read from the compiler): keeping
-              // that fragment live through it gives this one its own
-              if (i > 0) asm volatile("" ::"v"(ka), "v"(ka_prev));
-              ka_prev = ka;
+            if constexpr (kQ8) {
+              // dims block kb = i / 4: its hi MFMA in slot 4kb + 1, its lo
+              // MFMA in slot 4kb + 3; block kb + 1 read in slot 4kb
+              const int kb = i >> 2;
+              if ((i & 3) == 0 && kb + 1 < 9) k8[(kb + 1) % 3] = load_k8(kb + 1);
+              if ((i & 3) == 1) {
+                if (kb == 0) mfma_qk8<true>(sacc, k8[kb % 3], q8[2 * kb]);
+                else mfma_qk8<false>(sacc, k8[kb % 3], q8[2 * kb]);
+              }
+              if ((i & 3) == 3) mfma_qk8<false>(sacc, k8[kb % 3], q8[2 * kb + 1]);
+            } else {
+              bf16x8 ka;
+              if constexpr (LAT) ka = i < 32 ? fp8x8_scaled_to_bf16(kf[i % kKPre], tsc[i >> 3]) : kr[i & 3];
+              else ka = frag_bf16<FP8>(kf[i % kKPre]);
+              if constexpr (FP8) {
+                // the conversion must not reuse the registers of the MFMA just
+                // issued (the asm hides that read from the compiler): keeping
+                // that fragment live through it gives this one its own
+                if (i > 0) asm volatile("" ::"v"(ka), "v"(ka_prev));
+                ka_prev = ka;
+              }
+              if (i + kKPre < 36) {
+                if (LAT && i + kKPre >= 32) kr[(i + kKPre) & 3] = *(const bf16x8 LDS_AS*)(buf + kbase_r[(i + kKPre) & 3]);
+                else kf[i % kKPre] = load_k_raw<FP8>(buf, kbase, i + kKPre);
+              }
+              if (i == 0) mfma_qk<true, FP8>(sacc, ka, qf[i]);
+              else mfma_qk<false, FP8>(sacc, ka, qf[i]);
             }
-            if (i + kKPre < 36) {
-              if (LAT && i + kKPre >= 32) kr[(i + kKPre) & 3] = *(const bf16x8 LDS_AS*)(buf + kbase_r[(i + kKPre) & 3]);
-              else kf[i % kKPre] = load_k_raw<FP8>(buf, kbase, i + kKPre);
-            }
-            if (i == 0) mfma_qk<true, FP8>(sacc, ka, qf[i]);
-            else mfma_qk<false, FP8>(sacc, ka, qf[i]);
             if (q != kNone) {
               const int c = q >> 2, hb = q & 3;
               if constexpr (LAT) {
@@ -1600,7 +1714,7 @@ void attend_kernel(AttendLaunch a) {
             if (m_ref == -INFINITY) {
               float mx = -INFINITY;
 #pragma unroll
-              for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2);
+              for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r] * c2v);
               m_ref = fmaxf(mx, wave_xor32(mx));
             }
           }
@@ -1616,7 +1730,7 @@ void attend_kernel(AttendLaunch a) {
         float psum = 0.f, pexact = 0.f, plo = 0.f, tlo = 0.f;
         unsigned pb[8];
         auto softmax_elem = [&](int r) {
-          const float t = __builtin_fmaf(sacc[r], c2, -m_ref);
+          const float t = __builtin_fmaf(sacc[r], c2v, -m_ref);
           const float p = __builtin_amdgcn_exp2f(t);
           pexact += p;
           if (r & 1) {
