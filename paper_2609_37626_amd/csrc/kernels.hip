@@ -131,21 +131,24 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 raw) {
 
 __device__ __forceinline__ float wave_xor32(float v) { return __shfl_xor(v, 32, 64); }
 
-// ---- QK^T of the per-token fp8 cache on the fp8 matrix pipe.  A bf16
-// query value has 8 significant bits and an E4M3 code 4, so after scaling a
-// head's row by a power of two that puts its largest |q| in [128, 256), each
-// value x is the sum of two codes: hi = rne(x), then lo = rne(x - hi), whose
-// residual has at most 4 significant bits.  The split is exact for |x| >=
-// 1/4 (2^-10 of the row's largest value); below that the residual's lowest
-// bits fall under E4M3's smallest subnormal 2^-9, and each such term is off
-// by at most 2^-10, 2^-17 of the largest.  K enters as the cache's own codes.  S = scale * (K hi^T + K lo^T),
-// two 32x32x64 MFMAs per 64 dims, with no per-step conversion of K.
+// ---- QK^T of the fp8 caches on the fp8 matrix pipe.  A bf16 query value
+// has 8 significant bits and an E4M3 code 4, so after scaling a head's row
+// by a power of two that puts its largest |q| in [128, 256), each value x is
+// the sum of two codes: hi = rne(x), then lo = rne(x - hi), whose residual
+// has at most 4 significant bits.  lo holds the residual times 2^4 and its
+// MFMA scales it back by 2^-4 (the B operand's block scale), so the split is
+// exact for |x| >= 2^-6 (2^-14 of the row's largest value); below that each
+// term is off by at most 2^-14.  K enters as the cache's own codes (latent
+// rows: with each tile's power-of-two scale as the A operand's block
+// scale).  S = scale * (K hi^T + 2^-4 K lo^T), two 32x32x64 MFMAs per 64
+// dims, with no per-step conversion of K.
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 
 // 32 bf16 values of one 64-dim block (16 dwords: values 0-15 in `a`, 16-31
 // in `b`, two per dword, low half first) times `inv` -> hi codes into `a`,
-// lo codes into `b` (value v at byte v % 4 of dword v / 4).
+// lo codes (residual times 2^4) into `b` (value v at byte v % 4 of dword
+// v / 4).
 __device__ __forceinline__ void split_query_block(i32x8& a, i32x8& b, float inv) {
   i32x8 hi, lo;
 #pragma unroll
@@ -161,8 +164,8 @@ __device__ __forceinline__ void split_query_block(i32x8& a, i32x8& b, float inv)
     const f32x2 h01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(hw, 1.0f, false);
     const f32x2 h23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(hw, 1.0f, true);
     s16x2 v = {0, 0};
-    v = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(v, x0 - h01[0], x1 - h01[1], 1.0f, false);
-    v = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(v, x2 - h23[0], x3 - h23[1], 1.0f, true);
+    v = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(v, (x0 - h01[0]) * 16.f, (x1 - h01[1]) * 16.f, 1.0f, false);
+    v = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(v, (x2 - h23[0]) * 16.f, (x3 - h23[1]) * 16.f, 1.0f, true);
     hi[g] = hw;
     lo[g] = __builtin_bit_cast(int, v);
   }
@@ -170,15 +173,29 @@ __device__ __forceinline__ void split_query_block(i32x8& a, i32x8& b, float inv)
   b = lo;
 }
 
-// One 32x32x64 fp8 MFMA of the QK^T chain (VGPR accumulator, as mfma_qk).
-// K comes straight from LDS and the query codes were written at the unit's
-// start, so no VALU result feeds it.
-template <bool FIRST>
-__device__ __forceinline__ void mfma_qk8(f32x16& acc, const i32x8& k, const i32x8& q) {
-  if constexpr (FIRST)
-    asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, 0" : "=v"(acc) : "v"(k), "v"(q));
-  else
-    asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, %0" : "+v"(acc) : "v"(k), "v"(q));
+// One 32x32x64 fp8 MFMA of the QK^T chain (VGPR accumulator, as mfma_qk)
+// with E8M0 block scales: byte 0 of `ks` scales the lane's K block, byte 0
+// of `qs` its query block, each by 2^(byte - 127).  K comes straight from
+// LDS and the query codes were written at the unit's start; VALU_SRC adds
+// the wait states a scale written by the VALU just before needs (the
+// constant scales are opaque values made once, never rematerialised here).
+template <bool FIRST, bool VALU_SRC>
+__device__ __forceinline__ void mfma_qk8(f32x16& acc, const i32x8& k, const i32x8& q, int ks, int qs) {
+  if constexpr (FIRST) {
+    if constexpr (VALU_SRC)
+      asm volatile("s_nop 2\n\tv_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, 0, %3, %4 op_sel_hi:[0,0,0]"
+                   : "=v"(acc) : "v"(k), "v"(q), "v"(ks), "v"(qs));
+    else
+      asm volatile("v_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, 0, %3, %4 op_sel_hi:[0,0,0]"
+                   : "=v"(acc) : "v"(k), "v"(q), "v"(ks), "v"(qs));
+  } else {
+    if constexpr (VALU_SRC)
+      asm volatile("s_nop 2\n\tv_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0]"
+                   : "+v"(acc) : "v"(k), "v"(q), "v"(ks), "v"(qs));
+    else
+      asm volatile("v_mfma_scale_f32_32x32x64_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0]"
+                   : "+v"(acc) : "v"(k), "v"(q), "v"(ks), "v"(qs));
+  }
 }
 
 // ============================================================== planner ===
@@ -1174,8 +1191,11 @@ void attend_kernel(AttendLaunch a) {
   const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
   // per-token fp8 cache: QK on the fp8 matrix pipe with the query split in
   // two E4M3 terms; its power-of-two row scale joins the softmax constant
-  constexpr bool kQ8 = FP8 && !LAT;
+  constexpr bool kQ8 = FP8;
+  constexpr int kQB = LAT ? 8 : 9;  // 64-dim blocks on the fp8 pipe (latent rows: the RoPE 64 stay bf16)
   float c2v = c2;
+  // block scales of the fp8 QK MFMAs (E8M0): 1, and 2^-4 for the lo terms
+  const int bs_one = (int)opaque(127u), bs_lo = (int)opaque(127u - 4u);
   const uint8_t* __restrict__ kv = (const uint8_t*)a.kv;
   uint8_t LDS_AS* sm = (uint8_t LDS_AS*)smem;
   uint8_t LDS_AS* p_lds = sm + kPOff;
@@ -1294,14 +1314,19 @@ void attend_kernel(AttendLaunch a) {
   // split_query, q8[2kb] holds the hi codes of dims block kb, q8[2kb + 1] the
   // lo codes, in the byte order of the fp8 K operand)
   bf16x8 qf[kQ8 ? 1 : 36];
-  i32x8 q8[kQ8 ? 18 : 1];
+  i32x8 q8[kQ8 ? 2 * kQB : 1];
+  bf16x8 qr[LAT ? 4 : 1];  // latent rows: the RoPE fragments 32-35, bf16 (times the row scale's inverse)
   auto load_q = [&](int t) {
     const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)t * a.H + (head_ok ? head : 0)) * kDimQK + 8 * h;
     if constexpr (kQ8) {
 #pragma unroll
-      for (int m = 0; m < 18; ++m) {
+      for (int m = 0; m < 2 * kQB; ++m) {
         const u32x4 f0 = *(const u32x4*)(qrow + 32 * m), f1 = *(const u32x4*)(qrow + 32 * m + 16);
         q8[m] = __builtin_bit_cast(i32x8, __builtin_shufflevector(f0, f1, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      if constexpr (LAT) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) qr[p] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + 16 * (32 + p)));
       }
     } else {
 #pragma unroll
@@ -1311,21 +1336,39 @@ void attend_kernel(AttendLaunch a) {
   // kQ8: the head's row scale (lanes l and l ^ 32 hold its two halves), then
   // the split of every block; sets the lane's softmax constant
   auto split_query = [&]() {
+    auto bmax = [](float m, uint32_t w) {
+      return fmaxf(m, fmaxf(fabsf(__uint_as_float(w << 16)), fabsf(__uint_as_float(w & 0xFFFF0000u))));
+    };
     float mx = 0.f;
 #pragma unroll
-    for (int m = 0; m < 18; ++m)
+    for (int m = 0; m < 2 * kQB; ++m)
 #pragma unroll
-      for (int d = 0; d < 8; ++d) {
-        const uint32_t w = (uint32_t)q8[m][d];
-        mx = fmaxf(mx, fmaxf(fabsf(__uint_as_float(w << 16)), fabsf(__uint_as_float(w & 0xFFFF0000u))));
-      }
+      for (int d = 0; d < 8; ++d) mx = bmax(mx, (uint32_t)q8[m][d]);
+    if constexpr (LAT) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int d = 0; d < 4; ++d) mx = bmax(mx, __builtin_bit_cast(u32x4, qr[p])[d]);
+    }
     mx = fmaxf(mx, wave_xor32(mx));
     int e = (int)((__float_as_uint(mx) >> 23) & 255u) - 127;  // floor(log2 max), -127 for 0
     e = e < -100 ? -100 : (e > 120 ? 120 : e);
     const float inv = __uint_as_float((uint32_t)(127 + 7 - e) << 23);  // 2^(7 - e)
     c2v = c2 * __uint_as_float((uint32_t)(127 - 7 + e) << 23);         // c2 * 2^(e - 7)
 #pragma unroll
-    for (int kb = 0; kb < 9; ++kb) split_query_block(q8[2 * kb], q8[2 * kb + 1], inv);
+    for (int kb = 0; kb < kQB; ++kb) split_query_block(q8[2 * kb], q8[2 * kb + 1], inv);
+    if constexpr (LAT) {
+      // the RoPE fragments times the same power of two (exact in bf16)
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const u32x4 w = __builtin_bit_cast(u32x4, qr[p]);
+        u32x4 o;
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+          o[d] = pack_bf16x2(__uint_as_float(w[d] << 16) * inv, __uint_as_float(w[d] & 0xFFFF0000u) * inv);
+        qr[p] = __builtin_bit_cast(bf16x8, o);
+      }
+    }
   };
 
   i32x4 cur = unit_rec(0), nxt = unit_rec(1);
@@ -1535,6 +1578,11 @@ void attend_kernel(AttendLaunch a) {
           bf16x8 kr[4];    // LAT: the RoPE fragments, bf16 as staged
           f32x4 tsc;       // LAT: tile scales of this lane's key row
           if constexpr (LAT) tsc = *(const f32x4 LDS_AS*)(buf + L::kData + 16 * n32);
+          int tsb[4];  // LAT: the tile scales' E8M0 bytes (their biased exponents)
+          if constexpr (LAT) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) tsb[t] = (int)((__float_as_uint(tsc[t]) >> 23) & 255u);
+          }
           if constexpr (kQ8) {
             k8[0] = load_k8(0);
           } else {
@@ -1570,14 +1618,28 @@ void attend_kernel(AttendLaunch a) {
             }
             if constexpr (kQ8) {
               // dims block kb = i / 4: its hi MFMA in slot 4kb + 1, its lo
-              // MFMA in slot 4kb + 3; block kb + 1 read in slot 4kb
+              // MFMA (block scale 2^-4) in slot 4kb + 3; block kb + 1 read in
+              // slot 4kb.  Latent rows: K's block scale is its tile's, and the
+              // bf16 RoPE fragments (read in slots 28-31) take slots 32-35.
               const int kb = i >> 2;
-              if ((i & 3) == 0 && kb + 1 < 9) k8[(kb + 1) % 3] = load_k8(kb + 1);
-              if ((i & 3) == 1) {
-                if (kb == 0) mfma_qk8<true>(sacc, k8[kb % 3], q8[2 * kb]);
-                else mfma_qk8<false>(sacc, k8[kb % 3], q8[2 * kb]);
+              if ((i & 3) == 0 && kb + 1 < kQB) k8[(kb + 1) % 3] = load_k8(kb + 1);
+              if (kb < kQB) {
+                const int ksc = LAT ? tsb[kb >> 1] : bs_one;
+                if ((i & 3) == 1) {
+                  if (kb == 0) mfma_qk8<true, LAT>(sacc, k8[kb % 3], q8[2 * kb], ksc, bs_one);
+                  else mfma_qk8<false, false>(sacc, k8[kb % 3], q8[2 * kb], ksc, bs_one);
+                }
+                if ((i & 3) == 3) mfma_qk8<false, false>(sacc, k8[kb % 3], q8[2 * kb + 1], ksc, bs_lo);
               }
-              if ((i & 3) == 3) mfma_qk8<false>(sacc, k8[kb % 3], q8[2 * kb + 1]);
+              if constexpr (LAT) {
+                if (i >= 28 && i < 32) kr[i & 3] = *(const bf16x8 LDS_AS*)(buf + kbase_r[i & 3]);
+                if (i >= 32) {
+                  // the bf16 MFMA reads the accumulator the 16-pass fp8 MFMA
+                  // wrote: its wait states first
+                  if (i == 32) asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(sacc));
+                  mfma_qk<false, false>(sacc, kr[i & 3], qr[i & 3]);
+                }
+              }
             } else {
               bf16x8 ka;
               if constexpr (LAT) ka = i < 32 ? fp8x8_scaled_to_bf16(kf[i % kKPre], tsc[i >> 3]) : kr[i & 3];
