@@ -140,6 +140,22 @@ def test_many_split_rows_with_several_parts_each():
     assert_parity(batch, out, lse, label="merge by wave, 5-6 parts")
 
 
+def test_fp8_query_heads_of_very_different_magnitude():
+    """The fp8 caches run QK on the fp8 matrix pipe with each head's query
+    row scaled by its own power of two (its largest value into [128, 256))
+    and split in two E4M3 terms.  Heads scaled by 2^-12 .. 2^3 (exact bf16
+    exponent steps) must each meet the bar against the oracle on the same
+    scaled query, per-token cache and latent rows alike."""
+    for kv_dtype in (W.KV_FP8_E4M3, W.KV_FP8_LATENT):
+        batch = W.make_custom([700, 1500], H=128, q_chunk=2, kv_dtype=kv_dtype, seed=25)
+        q = batch.q.copy()
+        for hh in range(batch.H):
+            q[:, hh] = scale_bf16_bits(q[:, hh], hh % 16 - 12)
+        case = dataclasses.replace(batch, q=q)
+        out, lse = gpu_attend(case)
+        assert_parity(case, out, lse, label=f"fp8 query scales 2^-12..2^3, kv {kv_dtype}")
+
+
 def test_forced_splits_fp8_chunk():
     batch = W.make_custom([700, 2000], H=128, q_chunk=8, kv_dtype=W.KV_FP8_E4M3, seed=22)
     out, lse = gpu_attend(batch, flags=B.FLAG_FORCE_SPLIT, split_pages=4)
