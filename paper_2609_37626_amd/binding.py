@@ -28,6 +28,7 @@ KV_FP8_E4M3 = 1
 KV_FP8_LATENT = 2   # 656-byte rows: E4M3 latent, 4 fp32 tile scales, bf16 RoPE
 FLAG_DEBUG_CHECK = 1
 FLAG_FORCE_SPLIT = 2
+FLAG_EXACT_QK = 4
 DEFAULT_MAX_PARTIALS = 1024
 
 

@@ -233,6 +233,7 @@ int do_attend_units(const void* q, const void* kv_pages, const int32_t* block_ta
   a.kv_dtype = d->kv_dtype;
   a.B = d->batch;
   a.softmax_scale = d->softmax_scale;
+  a.exact_qk = (d->flags & SPLASH_FLAG_EXACT_QK) ? 1 : 0;
   a.ws = wv;
   hipError_t e = launch_attend(a, G, s);
   return e == hipSuccess ? SPLASH_OK : hip_fail(e, "attend launch");

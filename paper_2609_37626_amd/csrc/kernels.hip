@@ -1146,13 +1146,17 @@ __device__ __forceinline__ void pv_stream(const uint8_t LDS_AS* vbuf, const uint
 // covers list entries [64 p0, 64 p1) instead of pages, and its prologue
 // resolves every entry to its pool row (into the LDS the block-table slice
 // uses otherwise), from which each lane loads its staged row.
-// LAT: the fp8 latent-row cache (FP8 set too): latent tiles converted with
-// their tile scale for QK, the RoPE read as bf16, and for PV each wave's P
-// scaled by its tile's key scales.
-template <bool FP8, bool TOPK, bool LAT, bool NT>
+// LAT: the fp8 latent-row cache (FP8 set too): latent tiles with their tile
+// scale for QK, the RoPE read as bf16, and for PV each wave's P scaled by its
+// tile's key scales.
+// NT: non-temporal cache-row loads and result stores (one query row per
+// request).  Q8 (fp8 caches): QK on the fp8 matrix pipe (split query, K's
+// own codes); without it K is converted to bf16 for the bf16 MFMA.
+template <bool FP8, bool TOPK, bool LAT, bool NT, bool Q8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attend_kernel(AttendLaunch a) {
   static_assert(!LAT || FP8, "latent rows are an fp8 variant");
+  static_assert(!Q8 || FP8, "the fp8-pipe QK serves the fp8 caches");
   using L = StepLayout<FP8, LAT>;
   constexpr int kSlots = Ring<FP8, TOPK>::kSlots, kDist = Ring<FP8, TOPK>::kDist;
   constexpr int kRing = kSlots * L::kBuf;
@@ -1191,9 +1195,9 @@ void attend_kernel(AttendLaunch a) {
   const int head = 32 * wave + n32;
   const bool head_ok = head < a.H;
   const float c2 = a.softmax_scale * 1.4426950408889634f;  // log2(e)
-  // per-token fp8 cache: QK on the fp8 matrix pipe with the query split in
-  // two E4M3 terms; its power-of-two row scale joins the softmax constant
-  constexpr bool kQ8 = FP8;
+  // fp8 caches (Q8): QK on the fp8 matrix pipe with the query split in two
+  // E4M3 terms; its power-of-two row scale joins the softmax constant
+  constexpr bool kQ8 = Q8;
   constexpr int kQB = LAT ? 8 : 9;  // 64-dim blocks on the fp8 pipe (latent rows: the RoPE 64 stay bf16)
   float c2v = c2;
   // block scales of the fp8 QK MFMAs (E8M0): 1, and 2^-4 for the lo terms
@@ -2465,24 +2469,30 @@ hipError_t launch_plan(const PlanLaunch& p, hipStream_t s) {
 
 // NT (non-temporal cache-row loads) when every request has one query row:
 // then no two tiles read the same pages.
-template <bool FP8, bool TOPK, bool LAT>
+template <bool FP8, bool TOPK, bool LAT, bool Q8>
 static void launch_attend_nt(const AttendLaunch& a, int32_t workers, hipStream_t s) {
   if (a.q_chunk == 1)
-    hipLaunchKernelGGL((attend_kernel<FP8, TOPK, LAT, true>), dim3(workers), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attend_kernel<FP8, TOPK, LAT, true, Q8>), dim3(workers), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((attend_kernel<FP8, TOPK, LAT, false>), dim3(workers), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attend_kernel<FP8, TOPK, LAT, false, Q8>), dim3(workers), dim3(256), 0, s, a);
+}
+// fp8 caches: QK on the fp8 pipe unless the caller asked for the exact one
+template <bool TOPK, bool LAT>
+static void launch_attend_fp8(const AttendLaunch& a, int32_t workers, hipStream_t s) {
+  if (a.exact_qk) launch_attend_nt<true, TOPK, LAT, false>(a, workers, s);
+  else launch_attend_nt<true, TOPK, LAT, true>(a, workers, s);
 }
 
 hipError_t launch_attend(const AttendLaunch& a, int32_t workers, hipStream_t s) {
   if (a.kv_dtype == 2) {
-    if (a.topk_idx) launch_attend_nt<true, true, true>(a, workers, s);
-    else launch_attend_nt<true, false, true>(a, workers, s);
+    if (a.topk_idx) launch_attend_fp8<true, true>(a, workers, s);
+    else launch_attend_fp8<false, true>(a, workers, s);
   } else if (a.kv_dtype == 1) {
-    if (a.topk_idx) launch_attend_nt<true, true, false>(a, workers, s);
-    else launch_attend_nt<true, false, false>(a, workers, s);
+    if (a.topk_idx) launch_attend_fp8<true, false>(a, workers, s);
+    else launch_attend_fp8<false, false>(a, workers, s);
   } else {
-    if (a.topk_idx) launch_attend_nt<false, true, false>(a, workers, s);
-    else launch_attend_nt<false, false, false>(a, workers, s);
+    if (a.topk_idx) launch_attend_nt<false, true, false, false>(a, workers, s);
+    else launch_attend_nt<false, false, false, false>(a, workers, s);
   }
   return hipGetLastError();
 }

@@ -63,6 +63,7 @@ struct AttendLaunch {
   float* lse;
   int32_t bt_stride, q_chunk, H, kv_dtype, B;
   float softmax_scale;
+  int32_t exact_qk;  // fp8 caches: QK with K converted to bf16 (fp32-exact products), not on the fp8 pipe
   Workspace ws;
 };
 

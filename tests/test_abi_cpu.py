@@ -31,6 +31,13 @@ def test_header_declares_the_boundary():
         assert required in names
 
 
+def test_binding_flag_values_match_the_header():
+    text = open(HEADER).read()
+    values = {m.group(1): int(m.group(2)) for m in re.finditer(r"#define SPLASH_FLAG_(\w+)\s+(\d+)u", text)}
+    assert values == {"DEBUG_CHECK": B.FLAG_DEBUG_CHECK, "FORCE_SPLIT": B.FLAG_FORCE_SPLIT,
+                      "EXACT_QK": B.FLAG_EXACT_QK}
+
+
 def test_library_loads_and_exports_every_declared_symbol():
     raw = ctypes.CDLL(B.LIB_PATH)
     missing = [n for n in declared_functions() if not hasattr(raw, n)]

@@ -153,7 +153,12 @@ def test_fp8_query_heads_of_very_different_magnitude():
             q[:, hh] = scale_bf16_bits(q[:, hh], hh % 16 - 12)
         case = dataclasses.replace(batch, q=q)
         out, lse = gpu_attend(case)
-        assert_parity(case, out, lse, label=f"fp8 query scales 2^-12..2^3, kv {kv_dtype}")
+        ref_out, ref_lse = run_oracle(case)
+        assert_parity(case, out, lse, ref_out, ref_lse, label=f"fp8 query scales 2^-12..2^3, kv {kv_dtype}")
+        # SPLASH_FLAG_EXACT_QK: K converted to bf16, products summed in fp32
+        out_x, lse_x = gpu_attend(case, flags=B.FLAG_EXACT_QK)
+        assert_parity(case, out_x, lse_x, ref_out, ref_lse, label=f"  exact QK, kv {kv_dtype}")
+        assert np.abs(lse_x.cpu().numpy() - ref_lse).max() <= 5e-5
 
 
 def test_forced_splits_fp8_chunk():
