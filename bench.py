@@ -399,6 +399,8 @@ def main():
                          "ranks (pack its head slice, assemble its own rows, and back)")
     ap.add_argument("--dop-rows", type=int, default=0,
                     help="with --dop-ranks: current query rows N (default: the workload's B * q_chunk)")
+    ap.add_argument("--exact-qk", action="store_true",
+                    help="fp8 caches: QK with K converted to bf16 (SPLASH_FLAG_EXACT_QK) instead of the fp8 pipe")
     ap.add_argument("--kv-format", choices=["workload", "latent"], default="workload",
                     help="latent: the workload's lengths over the fp8 latent-row cache (656-byte rows)")
     ap.add_argument("--shards", type=int, default=0,
@@ -443,7 +445,7 @@ def main():
         return run_sharded(args, spec, batch, db)
     out, lse = db.alloc_outputs()
     ws = db.workspace()
-    desc = db.desc()
+    desc = db.desc(B.FLAG_EXACT_QK if args.exact_qk else 0)
     stream = torch.cuda.current_stream()
 
     def step_plain():
@@ -585,6 +587,8 @@ def main():
         "data": "synthetic (seeded PCG64 draws of the workload's length mix; N(0,1) cache rows and queries)",
         "config": {"workload": spec.name, "B": batch.B, "H": batch.H, "q_chunk": batch.q_chunk,
                    "lengths": list(spec.lengths), "kv_cache": W.KV_LABELS[batch.kv_dtype],
+                   "qk": "bf16 MFMA" if batch.kv_dtype == W.KV_BF16 else (
+                       "bf16 MFMA, K converted (exact)" if args.exact_qk else "fp8 MFMA, split query"),
                    "seed": spec.seed, "sum_seq_len": int(batch.seq_lens.sum()), "page_size": 64},
         "kv_gbps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
         "alg_gbps": round(alg_bytes / (us * 1e-6) / 1e9, 1),

@@ -85,7 +85,7 @@ extern "C" {
 /* fp8 caches (App. C: FP8 E4M3 KV): QK with K converted exactly to bf16 and
  * the bf16 MFMA's fp32 sums, instead of the default: K's own codes on the fp8
  * matrix pipe against the query split exactly into two E4M3 terms, faster
- * (config 5: about 15%) with sums kept to about 2^-18 of sum |q_i k_i|, so a
+ * (config 5: attend 629 against 722 us, latent rows 697 against 772) with sums kept to about 2^-18 of sum |q_i k_i|, so a
  * score is off by up to about 2^-18 * softmax_scale * sum |q_i k_i|.  No
  * effect on the bf16 cache. */
 #define SPLASH_FLAG_EXACT_QK     4u
